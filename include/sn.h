@@ -1,0 +1,183 @@
+/*
+ * sn.h -- C ABI of the stage-boundary subspace codec (Subspace Networks,
+ * arXiv 2506.01260), MI355X / gfx950.
+ *
+ * The operations (paper notation; rows are tokens, N = batch * seq):
+ *
+ *   compress        C   = (X - P[pos] - T_fixed[tok]) U       Sec. 4.3.1, Eq. (subtract)
+ *   decompress      X'  = C U^T + P[pos] + T_fixed[tok]       Sec. 4.3.1, recovery
+ *   grad compress   Cg  = G U                                  Sec. 4.4,  Eq. (grad_compress)
+ *   grad decompress G'  = Cg U^T   (sn_decompress, no tables)  Sec. 4.4,  recovery
+ *   project weights W  <- U (U^T W)  in place                  Sec. 4.3 / Sec. 5: the
+ *                   projection matrices' rows stay in S = Col(U); stored [out, in]
+ *                   (d x m), this projects every column of W.
+ *
+ * U (d x k) has orthonormal columns; T_fixed ("E", vocab x d) is the fixed
+ * high-rank token table and P (n_pos x d) the positional table that sender and
+ * receiver both hold (Sec. 4.3.1); tok / pos are the per-token ids.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - Every matrix is row-major; "ld" arguments are row strides in ELEMENTS.
+ * - All array pointers are DEVICE pointers (HIP device memory of the current
+ *   device) unless stated otherwise.  The library never allocates, frees or
+ *   keeps a pointer after a call returns; the caller owns every buffer.
+ * - dt (sn_dtype) is the element type of every float array of the call
+ *   (U, X, G, E, P, C, W): all SN_F32 or all SN_BF16.  Accumulation is fp32;
+ *   each output element is rounded once (round to nearest even) to dt.
+ * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and is
+ *   asynchronous: a return of SN_OK means "validated and launched".
+ * - N == 0 (or m == 0) is a valid no-op: SN_OK, nothing launched.
+ * - Errors are detected on the host before anything is launched and returned
+ *   as an sn_status; sn_last_error() gives a message for the calling thread.
+ *   SN_ERR_HIP reports a failed launch (message from hipGetErrorString).
+ * - Out-of-range token or position ids cannot be checked on the host (they
+ *   live in device memory): the kernels clamp them into range so no access
+ *   leaves the tables, and OR a bit into *err_flag (device int32, may be NULL):
+ *   bit 0 = a tok id outside [0, vocab), bit 1 = a pos id outside [0, n_pos).
+ *   The library never clears *err_flag; the caller zeroes it.
+ * - Results are bitwise deterministic: no floating-point atomics, fixed
+ *   reduction orders.
+ * - Calls are reentrant; calls on different streams that write the same
+ *   buffer race, as with any kernel.
+ */
+#ifndef SN_H_
+#define SN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sn_status {
+  SN_OK = 0,
+  SN_ERR_NULL = 1,         /* a required pointer is NULL                          */
+  SN_ERR_SHAPE = 2,        /* bad size, stride or id-range argument               */
+  SN_ERR_DTYPE = 3,        /* unknown dtype                                       */
+  SN_ERR_ALIGN = 4,        /* pointer not aligned to its element size / 256 B     */
+  SN_ERR_ALIAS = 5,        /* an output overlaps an input it may not overlap      */
+  SN_ERR_INDEX = 6,        /* reserved for bindings: set after reading err_flag   */
+  SN_ERR_HIP = 7,          /* a HIP runtime call or launch failed                 */
+  SN_ERR_UNSUPPORTED = 8,  /* valid but not implemented (e.g. k > SN_MAX_K)       */
+  SN_ERR_WORKSPACE = 9     /* workspace / packed buffer too small                 */
+} sn_status;
+
+typedef enum sn_dtype { SN_F32 = 0, SN_BF16 = 1 } sn_dtype;
+
+/* Largest supported rank k of the basis. */
+#define SN_MAX_K 256
+
+/* An opaque hipStream_t. */
+typedef void *sn_stream;
+
+/* ------------------------------------------------------------------------ */
+/* Packed basis.                                                              */
+/*                                                                            */
+/* U is shared by every stage and changes only when the subspace is updated   */
+/* (Sec. 4.5: a Grassmann step every few hundred iterations), so it is packed */
+/* once into the layouts the kernels read, and every codec call takes the     */
+/* packed buffer.  Re-pack after any change to U; a stale pack is not         */
+/* detected.                                                                  */
+/* ------------------------------------------------------------------------ */
+
+/* Size in bytes of the packed form of a d x k basis of element type dt
+ * (0 if the arguments are invalid).  Depends only on (d, k, dt). */
+size_t sn_basis_packed_bytes(int64_t d, int64_t k, int32_t dt);
+
+/* Pack U (d x k, row stride ldu >= k, element type dt) into `packed`
+ * (device buffer of at least sn_basis_packed_bytes(d, k, dt) bytes, 256-byte
+ * aligned).  U is read, `packed` fully written; they may not overlap.
+ * 1 <= k <= min(d, SN_MAX_K).  Errors: NULL, SHAPE, DTYPE, ALIGN, ALIAS,
+ * WORKSPACE, HIP. */
+int32_t sn_basis_pack(const void *U, int64_t d, int64_t k, int64_t ldu, int32_t dt,
+                      void *packed, size_t packed_bytes, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Forward codec.                                                             */
+/* ------------------------------------------------------------------------ */
+
+/* sn_compress: C[i, :] = (X[i, :] - P[pos_i, :] - E[tok[i], :]) U     (Sec. 4.3.1)
+ *
+ *   basis        packed basis of (d, k, dt)
+ *   X            N x d, row stride ldx >= d
+ *   tok          int32[N] token ids, or NULL when E is NULL
+ *   E            vocab x d token table T_fixed (row stride lde >= d), or NULL: no
+ *                token term
+ *   pos          int32[N] position ids, or NULL: pos_i = i mod seq_len
+ *   P            n_pos x d positional table (row stride ldp >= d), or NULL: no
+ *                positional term (pos and seq_len are then ignored)
+ *   seq_len      used only when P != NULL and pos == NULL; 1 <= seq_len <= n_pos
+ *   C            N x k output, row stride ldc >= k; may not overlap any input
+ *   err_flag     device int32 or NULL (see the header comment)
+ */
+int32_t sn_compress(const void *basis, int64_t d, int64_t k, int32_t dt,
+                    const void *X, int64_t N, int64_t ldx,
+                    const int32_t *tok, const void *E, int64_t vocab, int64_t lde,
+                    const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                    int64_t seq_len,
+                    void *C, int64_t ldc, int32_t *err_flag, sn_stream stream);
+
+/* sn_decompress: X[i, :] = C[i, :] U^T + P[pos_i, :] + E[tok[i], :]   (Sec. 4.3.1)
+ *
+ * Same argument meanings as sn_compress with C (N x k, ldc) the input and X
+ * (N x d, ldx) the output.  With E == NULL and P == NULL this is the gradient
+ * recovery G' = Cg U^T of Sec. 4.4.  X may not overlap any input. */
+int32_t sn_decompress(const void *basis, int64_t d, int64_t k, int32_t dt,
+                      const void *C, int64_t N, int64_t ldc,
+                      const int32_t *tok, const void *E, int64_t vocab, int64_t lde,
+                      const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                      int64_t seq_len,
+                      void *X, int64_t ldx, int32_t *err_flag, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Backward codec.                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* sn_grad_compress: Cg = G U   (Sec. 4.4, Eq. grad_compress; no embedding terms).
+ *   G   N x d activation gradient, row stride ldg >= d
+ *   Cg  N x k output, row stride ldc >= k; may not overlap G */
+int32_t sn_grad_compress(const void *basis, int64_t d, int64_t k, int32_t dt,
+                         const void *G, int64_t N, int64_t ldg,
+                         void *Cg, int64_t ldc, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Weight confinement.                                                        */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes sn_project_weights needs for a d x m matrix (0 if invalid). */
+size_t sn_project_weights_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t m);
+
+/* sn_project_weights: W <- U (U^T W), in place   (Sec. 4.3 and 5; Pi_S of App. E)
+ *
+ *   W          d x m, row stride ldw >= m, stored [out, in] (Wo: d x d,
+ *              W2: d x d_ff); every column is projected onto Col(U)
+ *   workspace  device buffer of at least
+ *              sn_project_weights_workspace_bytes(d, k, dt, m) bytes, 256-byte
+ *              aligned; holds T = U^T W (fp32) between the two passes.  Its
+ *              contents on entry are ignored and on exit are unspecified.
+ *   W is read completely before any element of it is written (stream order),
+ *   so the in-place update is safe.  The workspace may not overlap W. */
+int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt,
+                           void *W, int64_t m, int64_t ldw,
+                           void *workspace, size_t workspace_bytes, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Diagnostics.                                                               */
+/* ------------------------------------------------------------------------ */
+
+/* Static name of a status code. */
+const char *sn_status_string(int32_t status);
+
+/* Message for the last non-OK return on the calling thread ("" if none). */
+const char *sn_last_error(void);
+
+/* Library version string, e.g. "0.1.0 gfx950". */
+const char *sn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SN_H_ */

@@ -18,13 +18,17 @@ _BF16_MIN_QUANTUM_EXP = -133  # smallest subnormal 2**-133 = 2**(-126 - 7)
 _BF16_OVERFLOW = 2.0 ** 128   # first value past the largest finite bf16
 
 
-def decode_bf16(bits: np.ndarray) -> np.ndarray:
-    """uint16 bf16 bit patterns -> float64 (exact: bf16 is the top half of a float32)."""
+def decode_bf16(bits: np.ndarray, dtype=np.float64) -> np.ndarray:
+    """uint16 bf16 bit patterns -> float64 (or float32; both exact: bf16 is the
+    top half of a float32)."""
     b = np.asarray(bits)
     if b.dtype != np.uint16:
         b = b.astype(np.uint16)
+    f = (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    if dtype == np.float32:
+        return f
     with np.errstate(invalid="ignore"):
-        return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+        return f.astype(np.float64)
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:

@@ -60,9 +60,9 @@ def _embedding_terms(n, rows, tok, E, pos, P, seq_len):
     (P[pos[i]] or None, T_fixed[tok[i]] or None)."""
     pe = te = None
     if P is not None:
-        pe = _f64(P)[_positions(n, pos, P, seq_len)[rows]]
+        pe = _f64(np.asarray(P)[_positions(n, pos, P, seq_len)[rows]])
     if E is not None:
-        te = _f64(E)[_check_ids(tok, n, E.shape[0], "tok")[rows]]
+        te = _f64(np.asarray(E)[_check_ids(tok, n, E.shape[0], "tok")[rows]])
     return pe, te
 
 

@@ -1,0 +1,245 @@
+"""Python binding of the stage-boundary subspace codec (libsn.so, gfx950).
+
+Argument marshalling only: each function turns torch tensors into the plain
+pointers, sizes and strides of the C ABI in ``include/sn.h`` (same names) and
+launches on the current torch stream.  Every step of the codec runs in the
+library's HIP kernels; there is no fallback.  If the library has not been
+built the first call raises ``RuntimeError``.
+
+    basis = sn_basis_pack(U)                         # U: d x k, cuda, bf16 / fp32
+    C  = sn_compress(basis, X, tok=tok, E=E, P=P, seq_len=S)
+    Xr = sn_decompress(basis, C, tok=tok, E=E, P=P, seq_len=S)
+    Cg = sn_grad_compress(basis, G)
+    Gr = sn_decompress(basis, Cg)
+    sn_project_weights(basis, W)                     # in place
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsn.so")
+
+SN_F32, SN_BF16 = 0, 1
+SN_ERR_INDEX = 6
+STATUS = {0: "SN_OK", 1: "SN_ERR_NULL", 2: "SN_ERR_SHAPE", 3: "SN_ERR_DTYPE", 4: "SN_ERR_ALIGN",
+          5: "SN_ERR_ALIAS", 6: "SN_ERR_INDEX", 7: "SN_ERR_HIP", 8: "SN_ERR_UNSUPPORTED",
+          9: "SN_ERR_WORKSPACE"}
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "sn_basis_packed_bytes": (_SZ, [_I64, _I64, _I32]),
+    "sn_basis_pack": (_I32, [_P, _I64, _I64, _I64, _I32, _P, _SZ, _P]),
+    "sn_compress": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _P, _I64, _I64, _P, _P,
+                           _I64, _I64, _I64, _P, _I64, _P, _P]),
+    "sn_decompress": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _P, _I64, _I64, _P, _P,
+                             _I64, _I64, _I64, _P, _I64, _P, _P]),
+    "sn_grad_compress": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _I64, _P]),
+    "sn_project_weights_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
+    "sn_project_weights": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _SZ, _P]),
+    "sn_status_string": (ctypes.c_char_p, [_I32]),
+    "sn_last_error": (ctypes.c_char_p, []),
+    "sn_version": (ctypes.c_char_p, []),
+}
+
+
+class SnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        self.status = status
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+
+
+def lib():
+    """The loaded libsn.so (built by paper_2506_01260_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2506_01260_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise SnError(status, lib().sn_last_error().decode())
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SN_F32
+    if t.dtype == torch.bfloat16:
+        return SN_BF16
+    raise SnError(3, f"unsupported dtype {t.dtype}")
+
+
+def _torch_dtype(dt: int):
+    return torch.float32 if dt == SN_F32 else torch.bfloat16
+
+
+def _mat(t: torch.Tensor, name: str):
+    if not t.is_cuda:
+        raise SnError(2, f"{name} must be a device tensor")
+    if t.dim() != 2 or (t.shape[0] > 1 and t.stride(1) != 1) or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise SnError(2, f"{name} must be a 2-D row-major matrix (unit column stride)")
+    return t.data_ptr(), t.shape[0], t.shape[1], max(t.stride(0), t.shape[1])
+
+
+def _ids(t, name, n):
+    if t is None:
+        return None
+    if not t.is_cuda or t.dtype != torch.int32 or t.dim() != 1 or t.shape[0] != n or \
+            (n > 1 and t.stride(0) != 1):
+        raise SnError(2, f"{name} must be a contiguous int32 device vector of length {n}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Basis:
+    """A packed basis (the device buffer the codec calls read) plus its shape."""
+
+    def __init__(self, packed: torch.Tensor, d: int, k: int, dt: int):
+        self.packed, self.d, self.k, self.dt = packed, d, k, dt
+
+    @property
+    def ptr(self):
+        return self.packed.data_ptr()
+
+
+def sn_basis_packed_bytes(d: int, k: int, dt: int) -> int:
+    return lib().sn_basis_packed_bytes(d, k, dt)
+
+
+def sn_basis_pack(U: torch.Tensor, stream=None) -> Basis:
+    """Pack U (d x k) for the codec calls; re-pack whenever U changes."""
+    ptr, d, k, ldu = _mat(U, "U")
+    dt = _dt(U)
+    nbytes = sn_basis_packed_bytes(d, k, dt)
+    if nbytes == 0:
+        raise SnError(2, f"invalid basis shape {d} x {k}")
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=U.device)
+    _check(lib().sn_basis_pack(ptr, d, k, ldu, dt, packed.data_ptr(), nbytes, _stream(stream)))
+    return Basis(packed, d, k, dt)
+
+
+def _tables(N, tok, E, pos, P, seq_len):
+    e_ptr = vocab = lde = 0
+    if E is not None:
+        e_ptr, vocab, _, lde = _mat(E, "E")
+    p_ptr = n_pos = ldp = 0
+    if P is not None:
+        p_ptr, n_pos, _, ldp = _mat(P, "P")
+    tok_ptr = _ids(tok, "tok", N) if E is not None else None
+    pos_ptr = _ids(pos, "pos", N) if P is not None else None
+    return (tok_ptr, e_ptr or None, vocab, lde, pos_ptr, p_ptr or None, n_pos, ldp,
+            int(seq_len or 0))
+
+
+def _same_d(basis: Basis, d: int, *tables):
+    if d != basis.d:
+        raise SnError(2, f"matrix has {d} columns, basis has d = {basis.d}")
+    for name, t in tables:
+        if t is not None and (t.dim() != 2 or t.shape[1] != basis.d):
+            raise SnError(2, f"{name} must have d = {basis.d} columns")
+
+
+def _same_dtype(basis: Basis, *tensors):
+    for name, t in tensors:
+        if t is not None and _dt(t) != basis.dt:
+            raise SnError(3, f"{name} has dtype {t.dtype}; the basis was packed as "
+                             f"{_torch_dtype(basis.dt)}")
+
+
+def _out_shape(out, shape, name):
+    if tuple(out.shape) != tuple(shape):
+        raise SnError(2, f"{name} must have shape {tuple(shape)}, got {tuple(out.shape)}")
+
+
+def sn_compress(basis: Basis, X: torch.Tensor, tok=None, E=None, P=None, pos=None,
+                seq_len=None, out=None, err_flag=None, stream=None) -> torch.Tensor:
+    """C = (X - P[pos] - E[tok]) U."""
+    xp, N, d, ldx = _mat(X, "X")
+    _same_d(basis, d, ("E", E), ("P", P))
+    if out is None:
+        out = torch.empty((N, basis.k), dtype=_torch_dtype(basis.dt), device=X.device)
+    _out_shape(out, (N, basis.k), "out")
+    _same_dtype(basis, ("X", X), ("E", E), ("P", P), ("out", out))
+    cp, _, _, ldc = _mat(out, "out")
+    _check(lib().sn_compress(basis.ptr, basis.d, basis.k, basis.dt, xp, N, ldx,
+                             *_tables(N, tok, E, pos, P, seq_len), cp, ldc,
+                             None if err_flag is None else err_flag.data_ptr(), _stream(stream)))
+    return out
+
+
+def sn_decompress(basis: Basis, C: torch.Tensor, tok=None, E=None, P=None, pos=None,
+                  seq_len=None, out=None, err_flag=None, stream=None) -> torch.Tensor:
+    """X = C U^T + P[pos] + E[tok]; with no tables, the gradient recovery C U^T."""
+    cp, N, k, ldc = _mat(C, "C")
+    if k != basis.k:
+        raise SnError(2, f"C has {k} columns, basis has k = {basis.k}")
+    _same_d(basis, basis.d, ("E", E), ("P", P))
+    if out is None:
+        out = torch.empty((N, basis.d), dtype=_torch_dtype(basis.dt), device=C.device)
+    _out_shape(out, (N, basis.d), "out")
+    _same_dtype(basis, ("C", C), ("E", E), ("P", P), ("out", out))
+    xp, _, _, ldx = _mat(out, "out")
+    _check(lib().sn_decompress(basis.ptr, basis.d, basis.k, basis.dt, cp, N, ldc,
+                               *_tables(N, tok, E, pos, P, seq_len), xp, ldx,
+                               None if err_flag is None else err_flag.data_ptr(),
+                               _stream(stream)))
+    return out
+
+
+def sn_grad_compress(basis: Basis, G: torch.Tensor, out=None, stream=None) -> torch.Tensor:
+    """Cg = G U."""
+    gp, N, d, ldg = _mat(G, "G")
+    _same_d(basis, d)
+    if out is None:
+        out = torch.empty((N, basis.k), dtype=_torch_dtype(basis.dt), device=G.device)
+    _out_shape(out, (N, basis.k), "out")
+    _same_dtype(basis, ("G", G), ("out", out))
+    cp, _, _, ldc = _mat(out, "out")
+    _check(lib().sn_grad_compress(basis.ptr, basis.d, basis.k, basis.dt, gp, N, ldg, cp, ldc,
+                                  _stream(stream)))
+    return out
+
+
+def sn_project_weights_workspace_bytes(d: int, k: int, dt: int, m: int) -> int:
+    return lib().sn_project_weights_workspace_bytes(d, k, dt, m)
+
+
+def sn_project_weights(basis: Basis, W: torch.Tensor, workspace=None, stream=None) -> torch.Tensor:
+    """W <- U (U^T W) in place; returns W."""
+    wp, d, m, ldw = _mat(W, "W")
+    if d != basis.d:
+        raise SnError(2, f"W has {d} rows, basis has d = {basis.d}")
+    _same_dtype(basis, ("W", W))
+    need = sn_project_weights_workspace_bytes(basis.d, basis.k, basis.dt, m)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=W.device)
+    if workspace.numel() < need or not workspace.is_cuda:
+        raise SnError(9, f"workspace needs {need} device bytes")
+    _check(lib().sn_project_weights(basis.ptr, d, basis.k, basis.dt, wp, m, ldw,
+                                    workspace.data_ptr(), workspace.numel(), _stream(stream)))
+    return W
+
+
+def sn_version() -> str:
+    return lib().sn_version().decode()

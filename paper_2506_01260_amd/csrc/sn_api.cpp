@@ -1,0 +1,295 @@
+// The C ABI: host-side argument validation and dispatch to the kernels.
+// Every check runs before anything is launched; see include/sn.h for the
+// contract of each entry point.
+#include "sn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "sn_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int32_t fail(int32_t st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+int32_t ok() {
+  g_err[0] = '\0';
+  return SN_OK;
+}
+
+int32_t hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return ok();
+  return fail(SN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t elem_size(int32_t dt) { return dt == SN_F32 ? 4 : 2; }
+
+bool dtype_ok(int32_t dt) { return dt == SN_F32 || dt == SN_BF16; }
+
+bool elem_aligned(const void *p, int32_t dt) {
+  return (reinterpret_cast<uintptr_t>(p) & (elem_size(dt) - 1)) == 0;
+}
+
+// Byte range [lo, hi) covered by a rows x cols matrix with row stride ld.
+struct Span {
+  uintptr_t lo = 0, hi = 0;
+};
+
+Span span(const void *p, int64_t rows, int64_t cols, int64_t ld, size_t es) {
+  Span s;
+  if (!p || rows <= 0 || cols <= 0) return s;
+  s.lo = reinterpret_cast<uintptr_t>(p);
+  s.hi = s.lo + (static_cast<uintptr_t>(rows - 1) * ld + cols) * es;
+  return s;
+}
+
+bool overlap(Span a, Span b) { return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi; }
+
+constexpr int64_t kMaxDim = int64_t(1) << 31;  // rows, columns and strides stay below 2^31
+
+int32_t check_basis(const void *basis, int64_t d, int64_t k, int32_t dt) {
+  if (!dtype_ok(dt)) return fail(SN_ERR_DTYPE, "unknown dtype %d", dt);
+  if (!basis) return fail(SN_ERR_NULL, "basis is NULL");
+  if (reinterpret_cast<uintptr_t>(basis) & 255)
+    return fail(SN_ERR_ALIGN, "packed basis must be 256-byte aligned");
+  if (d < 1 || d >= kMaxDim) return fail(SN_ERR_SHAPE, "d = %lld out of range", (long long)d);
+  if (k < 1 || k > d) return fail(SN_ERR_SHAPE, "k = %lld must satisfy 1 <= k <= d", (long long)k);
+  if (k > SN_MAX_K) return fail(SN_ERR_UNSUPPORTED, "k = %lld > SN_MAX_K", (long long)k);
+  return SN_OK;
+}
+
+// Validates the id / table arguments shared by compress and decompress.
+int32_t check_ids(int64_t N, int64_t d, int32_t dt, const int32_t *tok, const void *E,
+                  int64_t vocab, int64_t lde, const int32_t *pos, const void *P, int64_t n_pos,
+                  int64_t ldp, int64_t seq_len) {
+  if (E) {
+    if (vocab < 1 || vocab >= kMaxDim)
+      return fail(SN_ERR_SHAPE, "vocab = %lld out of range", (long long)vocab);
+    if (lde < d || lde >= kMaxDim) return fail(SN_ERR_SHAPE, "lde must be >= d");
+    if (N > 0 && !tok) return fail(SN_ERR_NULL, "tok is NULL but E is given");
+    if (!elem_aligned(E, dt)) return fail(SN_ERR_ALIGN, "E not aligned to its element size");
+    if (tok && (reinterpret_cast<uintptr_t>(tok) & 3))
+      return fail(SN_ERR_ALIGN, "tok not 4-byte aligned");
+  }
+  if (P) {
+    if (n_pos < 1 || n_pos >= kMaxDim)
+      return fail(SN_ERR_SHAPE, "n_pos = %lld out of range", (long long)n_pos);
+    if (ldp < d || ldp >= kMaxDim) return fail(SN_ERR_SHAPE, "ldp must be >= d");
+    if (!pos && (seq_len < 1 || seq_len > n_pos))
+      return fail(SN_ERR_SHAPE, "pos is NULL: need 1 <= seq_len <= n_pos (seq_len = %lld)",
+                  (long long)seq_len);
+    if (!elem_aligned(P, dt)) return fail(SN_ERR_ALIGN, "P not aligned to its element size");
+    if (pos && (reinterpret_cast<uintptr_t>(pos) & 3))
+      return fail(SN_ERR_ALIGN, "pos not 4-byte aligned");
+  }
+  return SN_OK;
+}
+
+// The output span must not overlap any input span.
+int32_t check_out_alias(Span out, const void *basis, size_t basis_bytes, Span in, int64_t N,
+                        const int32_t *tok, const void *E, int64_t vocab, int64_t lde,
+                        const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                        int64_t d, size_t es) {
+  Span b;
+  b.lo = reinterpret_cast<uintptr_t>(basis);
+  b.hi = b.lo + basis_bytes;
+  if (overlap(out, b)) return fail(SN_ERR_ALIAS, "output overlaps the packed basis");
+  if (overlap(out, in)) return fail(SN_ERR_ALIAS, "output overlaps the input matrix");
+  if (E && overlap(out, span(E, vocab, d, lde, es)))
+    return fail(SN_ERR_ALIAS, "output overlaps E");
+  if (P && overlap(out, span(P, n_pos, d, ldp, es)))
+    return fail(SN_ERR_ALIAS, "output overlaps P");
+  if (E && tok && overlap(out, span(tok, 1, N, N, 4)))
+    return fail(SN_ERR_ALIAS, "output overlaps tok");
+  if (P && pos && overlap(out, span(pos, 1, N, N, 4)))
+    return fail(SN_ERR_ALIAS, "output overlaps pos");
+  return SN_OK;
+}
+
+sn::IdArgs make_ids(const int32_t *tok, const void *E, int64_t vocab, int64_t lde,
+                    const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                    int64_t seq_len, int32_t *err_flag) {
+  sn::IdArgs a;
+  a.E = E;
+  a.tok = E ? tok : nullptr;
+  a.vocab = vocab;
+  a.lde = lde;
+  a.P = P;
+  a.pos = P ? pos : nullptr;
+  a.n_pos = n_pos;
+  a.ldp = ldp;
+  a.seq_len = (P && !pos) ? seq_len : 1;
+  a.err_flag = err_flag;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t sn_basis_packed_bytes(int64_t d, int64_t k, int32_t dt) {
+  if (!dtype_ok(dt) || d < 1 || d >= kMaxDim || k < 1 || k > d || k > SN_MAX_K) return 0;
+  return sn::pack_layout(d, k, dt).total;
+}
+
+int32_t sn_basis_pack(const void *U, int64_t d, int64_t k, int64_t ldu, int32_t dt, void *packed,
+                      size_t packed_bytes, sn_stream stream) {
+  if (!dtype_ok(dt)) return fail(SN_ERR_DTYPE, "unknown dtype %d", dt);
+  if (!U || !packed) return fail(SN_ERR_NULL, "U or packed is NULL");
+  if (d < 1 || d >= kMaxDim) return fail(SN_ERR_SHAPE, "d out of range");
+  if (k < 1 || k > d) return fail(SN_ERR_SHAPE, "need 1 <= k <= d");
+  if (k > SN_MAX_K) return fail(SN_ERR_UNSUPPORTED, "k > SN_MAX_K");
+  if (ldu < k || ldu >= kMaxDim) return fail(SN_ERR_SHAPE, "ldu must be >= k");
+  if (!elem_aligned(U, dt)) return fail(SN_ERR_ALIGN, "U not aligned to its element size");
+  if (reinterpret_cast<uintptr_t>(packed) & 255)
+    return fail(SN_ERR_ALIGN, "packed must be 256-byte aligned");
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  if (packed_bytes < L.total)
+    return fail(SN_ERR_WORKSPACE, "packed buffer has %zu bytes, needs %zu", packed_bytes, L.total);
+  Span pu;
+  pu.lo = reinterpret_cast<uintptr_t>(packed);
+  pu.hi = pu.lo + L.total;
+  if (overlap(pu, span(U, d, k, ldu, elem_size(dt))))
+    return fail(SN_ERR_ALIAS, "packed overlaps U");
+  return hip_status(sn::launch_pack(L, U, ldu, packed, static_cast<hipStream_t>(stream)),
+                    "sn_basis_pack launch");
+}
+
+int32_t sn_compress(const void *basis, int64_t d, int64_t k, int32_t dt, const void *X, int64_t N,
+                    int64_t ldx, const int32_t *tok, const void *E, int64_t vocab, int64_t lde,
+                    const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                    int64_t seq_len, void *C, int64_t ldc, int32_t *err_flag, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (N < 0 || N >= kMaxDim) return fail(SN_ERR_SHAPE, "N = %lld out of range", (long long)N);
+  if (ldx < d || ldx >= kMaxDim) return fail(SN_ERR_SHAPE, "ldx must be >= d");
+  if (ldc < k || ldc >= kMaxDim) return fail(SN_ERR_SHAPE, "ldc must be >= k");
+  if ((st = check_ids(N, d, dt, tok, E, vocab, lde, pos, P, n_pos, ldp, seq_len))) return st;
+  if (N == 0) return ok();
+  if (!X || !C) return fail(SN_ERR_NULL, "X or C is NULL");
+  if (!elem_aligned(X, dt) || !elem_aligned(C, dt))
+    return fail(SN_ERR_ALIGN, "X or C not aligned to its element size");
+  const size_t es = elem_size(dt);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  if ((st = check_out_alias(span(C, N, k, ldc, es), basis, L.total, span(X, N, d, ldx, es), N,
+                            tok, E, vocab, lde, pos, P, n_pos, ldp, d, es)))
+    return st;
+  const sn::IdArgs ids = make_ids(tok, E, vocab, lde, pos, P, n_pos, ldp, seq_len, err_flag);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (sn::compress_mfma_ok(L, X, ldx, ids))
+    return hip_status(sn::launch_compress_mfma(L, basis, X, N, ldx, ids, C, ldc, s),
+                      "sn_compress launch");
+  return hip_status(sn::launch_compress_generic(L, basis, X, N, ldx, ids, C, ldc, s),
+                    "sn_compress launch");
+}
+
+int32_t sn_decompress(const void *basis, int64_t d, int64_t k, int32_t dt, const void *C,
+                      int64_t N, int64_t ldc, const int32_t *tok, const void *E, int64_t vocab,
+                      int64_t lde, const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                      int64_t seq_len, void *X, int64_t ldx, int32_t *err_flag,
+                      sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (N < 0 || N >= kMaxDim) return fail(SN_ERR_SHAPE, "N = %lld out of range", (long long)N);
+  if (ldx < d || ldx >= kMaxDim) return fail(SN_ERR_SHAPE, "ldx must be >= d");
+  if (ldc < k || ldc >= kMaxDim) return fail(SN_ERR_SHAPE, "ldc must be >= k");
+  if ((st = check_ids(N, d, dt, tok, E, vocab, lde, pos, P, n_pos, ldp, seq_len))) return st;
+  if (N == 0) return ok();
+  if (!X || !C) return fail(SN_ERR_NULL, "X or C is NULL");
+  if (!elem_aligned(X, dt) || !elem_aligned(C, dt))
+    return fail(SN_ERR_ALIGN, "X or C not aligned to its element size");
+  const size_t es = elem_size(dt);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  if ((st = check_out_alias(span(X, N, d, ldx, es), basis, L.total, span(C, N, k, ldc, es), N,
+                            tok, E, vocab, lde, pos, P, n_pos, ldp, d, es)))
+    return st;
+  const sn::IdArgs ids = make_ids(tok, E, vocab, lde, pos, P, n_pos, ldp, seq_len, err_flag);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (sn::decompress_mfma_ok(L, X, ldx, ids))
+    return hip_status(sn::launch_decompress_mfma(L, basis, C, N, ldc, ids, X, ldx, s),
+                      "sn_decompress launch");
+  return hip_status(sn::launch_decompress_generic(L, basis, C, N, ldc, ids, X, ldx, s),
+                    "sn_decompress launch");
+}
+
+int32_t sn_grad_compress(const void *basis, int64_t d, int64_t k, int32_t dt, const void *G,
+                         int64_t N, int64_t ldg, void *Cg, int64_t ldc, sn_stream stream) {
+  return sn_compress(basis, d, k, dt, G, N, ldg, nullptr, nullptr, 0, 0, nullptr, nullptr, 0, 0,
+                     0, Cg, ldc, nullptr, stream);
+}
+
+size_t sn_project_weights_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t m) {
+  if (!dtype_ok(dt) || d < 1 || d >= kMaxDim || k < 1 || k > d || k > SN_MAX_K || m < 0 ||
+      m >= kMaxDim)
+    return 0;
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  size_t a = sn::project_workspace_generic(d, k, m);
+  size_t b = L.mfma ? sn::project_workspace_mfma(d, k, m) : 0;
+  return sn::align256(a > b ? a : b);
+}
+
+int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt, void *W,
+                           int64_t m, int64_t ldw, void *workspace, size_t workspace_bytes,
+                           sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (m < 0 || m >= kMaxDim) return fail(SN_ERR_SHAPE, "m out of range");
+  if (ldw < m || ldw >= kMaxDim) return fail(SN_ERR_SHAPE, "ldw must be >= m");
+  if (m == 0) return ok();
+  if (!W || !workspace) return fail(SN_ERR_NULL, "W or workspace is NULL");
+  if (!elem_aligned(W, dt)) return fail(SN_ERR_ALIGN, "W not aligned to its element size");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    return fail(SN_ERR_ALIGN, "workspace must be 256-byte aligned");
+  const size_t need = sn_project_weights_workspace_bytes(d, k, dt, m);
+  if (workspace_bytes < need)
+    return fail(SN_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  Span w = span(W, d, m, ldw, elem_size(dt));
+  Span ws;
+  ws.lo = reinterpret_cast<uintptr_t>(workspace);
+  ws.hi = ws.lo + need;
+  Span b;
+  b.lo = reinterpret_cast<uintptr_t>(basis);
+  b.hi = b.lo + L.total;
+  if (overlap(w, ws) || overlap(w, b) || overlap(ws, b))
+    return fail(SN_ERR_ALIAS, "W, workspace and basis must not overlap");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (L.mfma && sn::project_mfma_ok(L, W, m, ldw))
+    return hip_status(sn::launch_project_mfma(L, basis, W, m, ldw, workspace, s),
+                      "sn_project_weights launch");
+  return hip_status(sn::launch_project_generic(L, basis, W, m, ldw, workspace, s),
+                    "sn_project_weights launch");
+}
+
+const char *sn_status_string(int32_t status) {
+  switch (status) {
+    case SN_OK: return "SN_OK";
+    case SN_ERR_NULL: return "SN_ERR_NULL";
+    case SN_ERR_SHAPE: return "SN_ERR_SHAPE";
+    case SN_ERR_DTYPE: return "SN_ERR_DTYPE";
+    case SN_ERR_ALIGN: return "SN_ERR_ALIGN";
+    case SN_ERR_ALIAS: return "SN_ERR_ALIAS";
+    case SN_ERR_INDEX: return "SN_ERR_INDEX";
+    case SN_ERR_HIP: return "SN_ERR_HIP";
+    case SN_ERR_UNSUPPORTED: return "SN_ERR_UNSUPPORTED";
+    case SN_ERR_WORKSPACE: return "SN_ERR_WORKSPACE";
+    default: return "SN_ERR_UNKNOWN";
+  }
+}
+
+const char *sn_last_error(void) { return g_err; }
+
+const char *sn_version(void) { return "0.1.0 gfx950"; }
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+// Host-side internals of the codec library: the packed-basis layout and the
+// kernel launchers the C ABI dispatches to.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sn {
+
+constexpr int kMaxK = 256;      // SN_MAX_K
+constexpr int kMfmaMaxKT = 8;   // MFMA path: k <= 128 (8 column tiles of 16)
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+// Packed basis (one device buffer, sections 256-byte aligned):
+//
+//  f32   U as float32, d x k, row stride k.  Read by the generic kernels.
+//  kfrag (bf16 and d % 32 == 0 and k <= 128 only) U in the MFMA operand layout
+//        of a contraction over d (compress, projection pass 1): 1 KiB blocks
+//        indexed [s][t], s = d/32 row steps, t = ceil(k/16) column tiles;
+//        lane l = 16 g + n of block (s, t) holds the 8 bf16
+//        U[32 s + 8 g + e, 16 t + n], e = 0..7 (0 past column k).
+//  rfrag (same condition) U in the MFMA operand layout of a contraction over k
+//        (decompress, projection pass 2): 1 KiB blocks indexed [p][h][q],
+//        p = d/32 row groups, h = 0..1, q = ceil(k/32) k-steps; lane
+//        l = 16 g + m holds the 8 bf16 U[32 p + 8 (m/4) + 4 h + m%4, 32 q + 8 g + e].
+//        The row order puts 8 consecutive d-rows of one token in one lane of
+//        the MFMA result, so decompress stores 16 bytes per lane.
+struct PackLayout {
+  int64_t d = 0, k = 0;
+  int dt = 0;
+  bool mfma = false;
+  int kt = 0;   // ceil(k/16)
+  int ks = 0;   // ceil(k/32)
+  size_t off_f32 = 0, off_kfrag = 0, off_rfrag = 0, total = 0;
+};
+
+PackLayout pack_layout(int64_t d, int64_t k, int dt);
+
+// ---- launchers (arguments already validated; N > 0) ----------------------
+struct IdArgs {
+  const int32_t *tok;
+  const void *E;
+  int64_t vocab, lde;
+  const int32_t *pos;
+  const void *P;
+  int64_t n_pos, ldp, seq_len;
+  int32_t *err_flag;
+};
+
+hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *packed,
+                       hipStream_t s);
+
+hipError_t launch_compress_generic(const PackLayout &L, const void *packed, const void *X,
+                                   int64_t N, int64_t ldx, const IdArgs &ids, void *C,
+                                   int64_t ldc, hipStream_t s);
+hipError_t launch_decompress_generic(const PackLayout &L, const void *packed, const void *C,
+                                     int64_t N, int64_t ldc, const IdArgs &ids, void *X,
+                                     int64_t ldx, hipStream_t s);
+
+size_t project_workspace_generic(int64_t d, int64_t k, int64_t m);
+hipError_t launch_project_generic(const PackLayout &L, const void *packed, void *W, int64_t m,
+                                  int64_t ldw, void *ws, hipStream_t s);
+
+// MFMA paths (bf16, L.mfma).  Return hipErrorNotSupported if the arguments do
+// not fit the fast path; the caller then uses the generic kernels.
+bool compress_mfma_ok(const PackLayout &L, const void *X, int64_t ldx, const IdArgs &ids);
+hipError_t launch_compress_mfma(const PackLayout &L, const void *packed, const void *X,
+                                int64_t N, int64_t ldx, const IdArgs &ids, void *C, int64_t ldc,
+                                hipStream_t s);
+bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs &ids);
+hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const void *C,
+                                  int64_t N, int64_t ldc, const IdArgs &ids, void *X,
+                                  int64_t ldx, hipStream_t s);
+
+size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m);
+bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw);
+hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *W, int64_t m,
+                               int64_t ldw, void *ws, hipStream_t s);
+
+}  // namespace sn

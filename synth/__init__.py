@@ -19,7 +19,10 @@ fp32 tensors as ``float32``.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
+import os
+
 import numpy as np
 
 ROW_BLOCK = 4096
@@ -106,14 +109,38 @@ def as_float(a: np.ndarray, dtype: str) -> np.ndarray:
 # Individual tensors
 # --------------------------------------------------------------------------
 
+def _workers() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _blocks(rows: int):
+    return list(enumerate(range(0, rows, ROW_BLOCK)))
+
+
+def _parallel(fn, items):
+    """Run fn over row blocks on a thread pool (numpy's generators and BLAS
+    release the GIL); each block has its own seed, so results do not depend on
+    the number of threads."""
+    with cf.ThreadPoolExecutor(max_workers=_workers()) as ex:
+        list(ex.map(fn, items))
+
+
 def gaussian(seed: int, rows: int, cols: int, std: float) -> np.ndarray:
     """float32 N(0, std^2) matrix drawn in ROW_BLOCK row blocks."""
     out = np.empty((rows, cols), dtype=np.float32)
-    for b, r0 in enumerate(range(0, rows, ROW_BLOCK)):
+
+    def one(item):
+        b, r0 = item
         r1 = min(rows, r0 + ROW_BLOCK)
         blk = _rng(seed, b).standard_normal((r1 - r0, cols), dtype=np.float32)
         blk *= np.float32(std)
         out[r0:r1] = blk
+
+    _parallel(one, _blocks(rows))
     return out
 
 
@@ -181,33 +208,40 @@ def make_activations(cfg_id: int, basis: dict, emb: dict, ids: dict,
     This synthesises activations with the structure the paper derives for a
     subspace network (Section 4.2: the residual stream minus the embedding
     terms lies in span(U)); eta_perp is Gaussian noise with its span(U)
-    component removed, so it is pure off-subspace residual.  Built in float64
-    per row block.  Returns X (stored), C_true (float64) and the float64
+    component removed, so it is pure off-subspace residual.  Built per row
+    block in float64 for fp32 configs and float32 for bf16 configs (far below
+    bf16's rounding).  Returns X (stored), C_true (float64) and the norm of the
     off-subspace noise actually added (before the final rounding of X).
     """
     cfg = cfg or CONFIGS[cfg_id]
     sigma = cfg.sigma if sigma is None else sigma
+    ft = np.float64 if cfg.dtype == "f32" else np.float32
     tok, pos = ids["tok"], ids["pos"]
     n = tok.shape[0]
-    U = as_float(basis["U"], cfg.dtype).astype(np.float64)   # the stored basis
-    Ef = as_float(emb["E"], cfg.dtype)
-    Pf = as_float(emb["P"], cfg.dtype)
+    U = as_float(basis["U"], cfg.dtype).astype(ft)   # the stored basis
+    Eb, Pb = emb["E"], emb["P"]
     C_true = np.empty((n, cfg.k), dtype=np.float64)
     X = np.empty((n, cfg.d), dtype=np.float32 if cfg.dtype == "f32" else np.uint16)
-    noise_sq = 0.0
-    for b, r0 in enumerate(range(0, n, ROW_BLOCK)):
+    noise_sq = np.zeros(len(_blocks(n)))
+
+    def one(item):
+        b, r0 = item
         r1 = min(n, r0 + ROW_BLOCK)
         c = _rng(seed_of(cfg_id, ORD_C), b).standard_normal((r1 - r0, cfg.k))
         C_true[r0:r1] = c
-        blk = Ef[tok[r0:r1]].astype(np.float64) + Pf[pos[r0:r1]].astype(np.float64)
-        blk += c @ U.T
+        blk = as_float(Eb[tok[r0:r1]], cfg.dtype).astype(ft)
+        blk += as_float(Pb[pos[r0:r1]], cfg.dtype)
+        blk += c.astype(ft) @ U.T
         if sigma > 0:
-            eta = _rng(seed_of(cfg_id, ORD_NOISE), b).standard_normal((r1 - r0, cfg.d)) * sigma
+            eta = _rng(seed_of(cfg_id, ORD_NOISE), b).standard_normal((r1 - r0, cfg.d), dtype=ft)
+            eta *= ft(sigma)
             eta -= (eta @ U) @ U.T
-            noise_sq += float(np.sum(eta * eta))
+            noise_sq[b] = float(np.sum(eta.astype(np.float64) ** 2))
             blk += eta
         X[r0:r1] = store(blk, cfg.dtype)
-    return {"X": X, "C_true": C_true, "noise_norm": noise_sq ** 0.5}
+
+    _parallel(one, _blocks(n))
+    return {"X": X, "C_true": C_true, "noise_norm": float(np.sum(noise_sq)) ** 0.5}
 
 
 def make_gradient(cfg_id: int, n: int | None = None, cfg: Config | None = None) -> np.ndarray:
@@ -220,6 +254,17 @@ def make_weight(cfg_id: int, index: int, rows: int, cols: int,
                 cfg: Config | None = None) -> np.ndarray:
     cfg = cfg or CONFIGS[cfg_id]
     return store(gaussian(seed_of(cfg_id, ORD_W + index), rows, cols, 0.02), cfg.dtype)
+
+
+def device_weight(cfg_id: int, index: int, rows: int, cols: int, std: float = 0.02,
+                  device: str = "cuda"):
+    """A bf16 N(0, std^2) weight matrix drawn directly on the device with torch's
+    seeded generator (for sweeps too large to draw on the host)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed_of(cfg_id, ORD_W + index))
+    w = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32)
+    return (w * std).to(torch.bfloat16)
 
 
 def make_workload(cfg_id: int, n: int | None = None, sigma: float | None = None) -> dict:

@@ -1,0 +1,119 @@
+"""The C-ABI library on the host (no GPU): it loads, exports every entry point
+include/sn.h declares, and rejects invalid arguments before any launch.
+
+Every call here fails validation (or is an N == 0 no-op), so nothing touches a
+device; the pointers are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2506_01260_amd as sn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sn.h")
+FAKE = 0x7F0000000000            # a 256-byte-aligned address that is never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(sn_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 10
+    L = ctypes.CDLL(sn.LIB_PATH)
+    for name in names:
+        assert hasattr(L, name), f"{name} declared in sn.h but not exported"
+    assert set(names) == set(sn._SIGNATURES), "binding and header disagree"
+    assert sn.sn_version().endswith("gfx950")
+
+
+def test_status_strings():
+    L = sn.lib()
+    assert L.sn_status_string(0) == b"SN_OK"
+    for code, name in sn.STATUS.items():
+        assert L.sn_status_string(code).decode() == name
+
+
+def test_packed_and_workspace_sizes():
+    assert sn.sn_basis_packed_bytes(4096, 40, 1) > 4096 * 40 * 4
+    assert sn.sn_basis_packed_bytes(4096, 40, 1) % 256 == 0
+    assert sn.sn_basis_packed_bytes(4096, 0, 1) == 0
+    assert sn.sn_basis_packed_bytes(8, 9, 1) == 0          # k > d
+    assert sn.sn_basis_packed_bytes(4096, 40, 7) == 0      # bad dtype
+    assert sn.sn_basis_packed_bytes(4096, 257, 1) == 0     # k > SN_MAX_K
+    assert sn.lib().sn_project_weights_workspace_bytes(4096, 40, 1, 4096) > 0
+
+
+def _compress(**over):
+    a = dict(basis=FAKE, d=256, k=8, dt=1, X=FAKE + (1 << 20), N=16, ldx=256, tok=FAKE + (2 << 20),
+             E=FAKE + (3 << 20), vocab=10, lde=256, pos=None, P=None, n_pos=0, ldp=0,
+             seq_len=0, C=FAKE + (8 << 20), ldc=8, err=None, stream=None)
+    a.update(over)
+    return sn.lib().sn_compress(a["basis"], a["d"], a["k"], a["dt"], a["X"], a["N"], a["ldx"],
+                                a["tok"], a["E"], a["vocab"], a["lde"], a["pos"], a["P"],
+                                a["n_pos"], a["ldp"], a["seq_len"], a["C"], a["ldc"], a["err"],
+                                a["stream"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(basis=None), 1),
+    (dict(basis=FAKE + 16), 4),                 # packed basis not 256-aligned
+    (dict(dt=5), 3),
+    (dict(k=0), 2), (dict(k=300, d=512), 8), (dict(k=9, d=8, ldx=8), 2),
+    (dict(N=-1), 2), (dict(ldx=255), 2), (dict(ldc=7), 2),
+    (dict(tok=None), 1),                         # E given without ids
+    (dict(vocab=0), 2), (dict(lde=100), 2),
+    (dict(P=FAKE + (4 << 20), n_pos=4, ldp=256, seq_len=0), 2),   # default pos needs seq_len
+    (dict(P=FAKE + (4 << 20), n_pos=4, ldp=256, seq_len=5), 2),   # seq_len > n_pos
+    (dict(X=None), 1), (dict(C=None), 1),
+    (dict(X=FAKE + 1), 4),                       # misaligned bf16 pointer
+    (dict(C=FAKE + (1 << 20) + 64), 5),          # C overlaps X
+    (dict(C=FAKE + (3 << 20)), 5),               # C overlaps E
+    (dict(C=FAKE + 512), 5),                     # C overlaps the packed basis
+])
+def test_compress_rejects_invalid_arguments(over, code):
+    assert _compress(**over) == code
+    assert sn.lib().sn_last_error().decode() != ""
+
+
+def test_empty_batch_returns_ok_without_launch():
+    assert _compress(N=0, X=None, C=None) == 0
+
+
+def test_decompress_and_projection_validation():
+    L = sn.lib()
+    # decompress: output overlapping its input C
+    st = L.sn_decompress(FAKE, 256, 8, 1, FAKE + (1 << 20), 16, 8, None, None, 0, 0, None, None,
+                         0, 0, 0, FAKE + (1 << 20), 256, None, None)
+    assert st == 5
+    st = L.sn_grad_compress(FAKE, 256, 8, 1, FAKE + (1 << 20), 16, 100, FAKE + (8 << 20), 8, None)
+    assert st == 2                                # ldg < d
+    # projection: workspace too small, misaligned, overlapping, m == 0
+    need = L.sn_project_weights_workspace_bytes(256, 8, 1, 64)
+    st = L.sn_project_weights(FAKE, 256, 8, 1, FAKE + (1 << 20), 64, 64, FAKE + (8 << 20),
+                              need - 1, None)
+    assert st == 9
+    st = L.sn_project_weights(FAKE, 256, 8, 1, FAKE + (1 << 20), 64, 64, FAKE + (8 << 20) + 8,
+                              need, None)
+    assert st == 4
+    st = L.sn_project_weights(FAKE, 256, 8, 1, FAKE + (1 << 20), 64, 64, FAKE + (1 << 20),
+                              need, None)
+    assert st == 5
+    assert L.sn_project_weights(FAKE, 256, 8, 1, None, 0, 0, None, 0, None) == 0
+    # pack: too small a buffer, misaligned target
+    assert L.sn_basis_pack(FAKE + (1 << 20), 256, 8, 8, 1, FAKE, 100, None) == 9
+    assert L.sn_basis_pack(FAKE + (1 << 20), 256, 8, 8, 1, FAKE + 8, 1 << 20, None) == 4
+    assert L.sn_basis_pack(FAKE + (1 << 20), 256, 8, 4, 1, FAKE, 1 << 20, None) == 2
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    U = torch.zeros(64, 8, dtype=torch.bfloat16)
+    with pytest.raises(sn.SnError):
+        sn.sn_basis_pack(U)

@@ -1,0 +1,448 @@
+"""GPU parity of the HIP codec (through the C ABI) against the CPU oracle.
+
+Inputs come from the seeded generator (``synth``) or are designed here; every
+expected value comes from ``oracle`` (float64, rounded once to the output
+dtype) or from the stored exact fixture.  Nothing the GPU produces is fed to
+the oracle.  Large configs compare sampled rows / columns, which the oracle
+computes one by one; small cases compare everything.
+"""
+from __future__ import annotations
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2506_01260_amd as sn
+from gpu_helpers import assert_parity, dev, host, host_bits, ids, log
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "tiny_exact.json")
+
+_CACHE: dict = {}
+
+
+def workload(cfg: int, n: int | None = None, sigma: float | None = None) -> dict:
+    key = (cfg, n, sigma)
+    if key not in _CACHE:
+        log(f"[gen] config {cfg} n={n} sigma={sigma}")
+        _CACHE.clear()  # keep host memory bounded: one workload at a time
+        _CACHE[key] = synth.make_workload(cfg, n, sigma)
+    return _CACHE[key]
+
+
+def oracle_inputs(w: dict) -> dict:
+    """Exact float32 views of the stored inputs (the oracle up-converts the
+    rows it uses to float64)."""
+    dt = w["cfg"].dtype
+    if dt == "bf16":
+        dec = lambda a: oracle.decode_bf16(a, np.float32)  # noqa: E731
+    else:
+        dec = lambda a: np.asarray(a, np.float32)  # noqa: E731
+    out = {name: dec(w[name]) for name in ("E", "P", "X", "G")}
+    out["U"] = dec(w["U"]).astype(np.float64)
+    return out
+
+
+def host_rows(t: torch.Tensor, sel: np.ndarray) -> np.ndarray:
+    return host(t[torch.from_numpy(np.asarray(sel, dtype=np.int64)).cuda()])
+
+
+def sample_rows(n: int, count: int, seed: int) -> np.ndarray:
+    rng = np.random.default_rng(seed)
+    edge = np.r_[np.arange(min(n, 48)), np.arange(max(0, n - 48), n)]
+    return np.unique(np.r_[edge, rng.integers(0, n, size=min(count, n))])
+
+
+def run_codec(w: dict, rows: np.ndarray | None, tag: str):
+    """Forward and gradient codec of workload w on the GPU vs the oracle."""
+    cfg = w["cfg"]
+    dt = cfg.dtype
+    o = oracle_inputs(w)
+    U = dev(w["U"], dt)
+    basis = sn.sn_basis_pack(U)
+    X, E, P, G = dev(w["X"], dt), dev(w["E"], dt), dev(w["P"], dt), dev(w["G"], dt)
+    tok = ids(w["tok"])
+    n = w["tok"].shape[0]
+    sel = np.arange(n) if rows is None else rows
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    log(f"[{tag}] compress N={n} d={cfg.d} k={cfg.k} {dt}")
+    C = sn.sn_compress(basis, X, tok=tok, E=E, P=P, seq_len=cfg.seq, err_flag=flag)
+    ref = oracle.round_to(oracle.compress(o["X"], o["U"], w["tok"], o["E"], o["P"],
+                                          seq_len=cfg.seq, rows=sel), dt)
+    assert_parity(host(C)[sel], ref, dt, f"{tag} compress")
+
+    # decompress of generator coefficients (same input on both sides)
+    Cin_np = synth.store(w["C_true"], dt)
+    Cin = dev(Cin_np, dt)
+    Cin64 = oracle.decode_bf16(Cin_np) if dt == "bf16" else Cin_np.astype(np.float64)
+    log(f"[{tag}] decompress")
+    Xr = sn.sn_decompress(basis, Cin, tok=tok, E=E, P=P, seq_len=cfg.seq, err_flag=flag)
+    ref = oracle.round_to(oracle.decompress(Cin64, o["U"], w["tok"], o["E"], o["P"],
+                                            seq_len=cfg.seq, rows=sel), dt)
+    assert_parity(host_rows(Xr, sel), ref, dt, f"{tag} decompress")
+
+    log(f"[{tag}] grad compress / decompress")
+    Cg = sn.sn_grad_compress(basis, G)
+    ref = oracle.round_to(oracle.grad_compress(o["G"], o["U"], rows=sel), dt)
+    assert_parity(host(Cg)[sel], ref, dt, f"{tag} grad_compress")
+    Gr = sn.sn_decompress(basis, Cin)
+    ref = oracle.round_to(oracle.grad_decompress(Cin64, o["U"], rows=sel), dt)
+    assert_parity(host_rows(Gr, sel), ref, dt, f"{tag} grad_decompress")
+
+    # property at any size: the forward round trip loses only the off-subspace
+    # residual (plus rounding of C and X_rec to the dtype)
+    Xrt = host_rows(sn.sn_decompress(basis, C, tok=tok, E=E, P=P, seq_len=cfg.seq), sel)
+    Xh = o["X"][sel].astype(np.float64)
+    err = np.linalg.norm(Xrt - Xh)
+    emb = o["E"][w["tok"][sel]].astype(np.float64) + o["P"][(sel % cfg.seq)]
+    resid = Xh - emb
+    off = np.linalg.norm(resid - (resid @ o["U"]) @ o["U"].T)
+    scale = np.linalg.norm(Xh)
+    slack = (1e-5 if dt == "f32" else 2e-2) * scale
+    log(f"[{tag}] round trip |X_rec - X| = {err:.4g}, off-subspace {off:.4g}, |X| {scale:.4g}")
+    assert abs(err - off) <= slack
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 0, "no id is out of range in generated workloads"
+
+
+# ---------------------------------------------------------------- fixtures
+
+def _golden(d_pad: int, dtype: str):
+    g = json.load(open(GOLDEN))
+    d = g["d"]
+    f = lambda m: np.array([[float(Fraction(v)) for v in r] for r in m])  # noqa: E731
+
+    def pad(a):
+        out = np.zeros((a.shape[0], d_pad))
+        out[:, :d] = a
+        return out
+
+    mats = {n: f(g[n]) for n in ("U", "E", "P", "X", "G")}
+    mats = {n: pad(a.T).T if n == "U" else pad(a) for n, a in mats.items()}
+    mats["U"] = mats["U"]  # d_pad x k, zero rows past d
+    W = np.zeros((d_pad, 6))
+    W[:d] = f(g["W"])
+    mats["W"] = W
+    ex = {n: f(v) for n, v in g["expect"].items()}
+    ex["X_rec"] = pad(ex["X_rec"])
+    ex["G_rec"] = pad(ex["G_rec"])
+    Wp = np.zeros((d_pad, 6))
+    Wp[:d] = ex["W_proj"]
+    ex["W_proj"] = Wp
+    return g, mats, ex
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d_pad", [8, 32, 64])
+def test_golden_fixture_exact(dtype, d_pad):
+    """Dyadic inputs whose exact results every dtype represents: bit-exact."""
+    log(f"[golden] dtype={dtype} d={d_pad}")
+    g, m, ex = _golden(d_pad, dtype)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    t = {n: torch.tensor(a, dtype=tdt, device="cuda") for n, a in m.items()}
+    basis = sn.sn_basis_pack(t["U"])
+    tok, pos = ids(np.array(g["tok"])), ids(np.array(g["pos"]))
+    C = sn.sn_compress(basis, t["X"], tok=tok, E=t["E"], P=t["P"], pos=pos)
+    assert np.array_equal(host(C), ex["C"])
+    Xr = sn.sn_decompress(basis, C, tok=tok, E=t["E"], P=t["P"], pos=pos)
+    assert np.array_equal(host(Xr), ex["X_rec"])
+    Cg = sn.sn_grad_compress(basis, t["G"])
+    assert np.array_equal(host(Cg), ex["Cg"])
+    assert np.array_equal(host(sn.sn_decompress(basis, Cg)), ex["G_rec"])
+    W = t["W"].clone()
+    sn.sn_project_weights(basis, W)
+    assert np.array_equal(host(W), ex["W_proj"])
+
+
+# ------------------------------------------------------------ the configs
+
+@pytest.mark.parametrize("sigma", [0.0, 1e-3])
+def test_config0_fp32_all_ops(sigma):
+    w = workload(0, sigma=sigma)
+    run_codec(w, None, f"cfg0 sigma={sigma}")
+    cfg = w["cfg"]
+    (rows, cols), = cfg.weights
+    Wnp = synth.make_weight(0, 0, rows, cols)
+    W = dev(Wnp, "f32")
+    basis = sn.sn_basis_pack(dev(w["U"], "f32"))
+    sn.sn_project_weights(basis, W)
+    ref = oracle.round_to(oracle.project_weights(Wnp.astype(np.float64),
+                                                 w["U"].astype(np.float64)), "f32")
+    assert_parity(host(W), ref, "f32", "cfg0 project_weights")
+
+
+def test_config1_bf16_full():
+    run_codec(workload(1), None, "cfg1")
+
+
+def test_config2_bf16_sampled():
+    w = workload(2)
+    run_codec(w, sample_rows(w["tok"].shape[0], 1024, 2), "cfg2")
+
+
+@pytest.mark.parametrize("n", [32768, 32767])
+def test_config4_bf16_sampled(n):
+    w = workload(4, n=n)
+    run_codec(w, sample_rows(n, 512, 4), f"cfg4 N={n}")
+
+
+def _project_check(cfg_id: int, basis, U64: np.ndarray, W: torch.Tensor, tag: str, seed: int):
+    """Project W on the GPU and compare sampled columns with the oracle."""
+    m = W.shape[1]
+    rng = np.random.default_rng(seed)
+    cols = np.unique(np.r_[np.arange(min(m, 16)), np.arange(max(0, m - 16), m),
+                           rng.integers(0, m, 96)])
+    before = host(W[:, torch.from_numpy(cols).cuda()])
+    sn.sn_project_weights(basis, W)
+    after = host(W[:, torch.from_numpy(cols).cuda()])
+    ref = oracle.round_to(oracle.project_weights(before, U64), "bf16")
+    assert_parity(after.T, ref.T, "bf16", f"{tag} project_weights (columns as rows)")
+    # invariants on the GPU result: U^T W' = U^T W, and W' has no off-subspace part
+    t_before = U64.T @ before
+    t_after = U64.T @ after
+    assert np.linalg.norm(t_after - t_before) <= 1e-2 * np.linalg.norm(t_before)
+    resid = after - U64 @ t_after
+    assert np.linalg.norm(resid) <= 1e-2 * np.linalg.norm(after)
+
+
+@pytest.mark.parametrize("cfg_id", [2, 4])
+def test_project_weights_configs(cfg_id):
+    cfg = synth.CONFIGS[cfg_id]
+    b = synth.make_basis(cfg_id)
+    U64 = oracle.decode_bf16(b["U"])
+    basis = sn.sn_basis_pack(dev(b["U"], "bf16"))
+    for i, (rows, cols) in enumerate(cfg.weights):
+        log(f"[cfg{cfg_id}] project W{i} {rows}x{cols}")
+        W = dev(synth.make_weight(cfg_id, i, rows, cols), "bf16")
+        _project_check(cfg_id, basis, U64, W, f"cfg{cfg_id} W{i}", seed=10 + i)
+
+
+def test_config3_layer_sweep():
+    """32 layers x (Wo, W2) projected in place; weights drawn on the device
+    (seeded) to keep host memory small."""
+    cfg = synth.CONFIGS[3]
+    b = synth.make_basis(3)
+    U64 = oracle.decode_bf16(b["U"])
+    basis = sn.sn_basis_pack(dev(b["U"], "bf16"))
+    for layer in range(cfg.layers):
+        for i, (rows, cols) in enumerate(cfg.weights):
+            W = synth.device_weight(3, 2 * layer + i, rows, cols)
+            if layer % 8 == 0 or layer == cfg.layers - 1:
+                log(f"[cfg3] layer {layer} W{i} {rows}x{cols}")
+                _project_check(3, basis, U64, W, f"cfg3 L{layer} W{i}", seed=100 * layer + i)
+            else:
+                sn.sn_project_weights(basis, W)
+            del W
+
+
+# --------------------------------------------------------------- edge cases
+
+def _small(d, k, n, vocab=50, seq=9, dtype="bf16", seed=0, grid=None):
+    rng = np.random.default_rng(seed)
+    U, _ = np.linalg.qr(rng.standard_normal((d, k)))
+    E = rng.standard_normal((vocab, d)) * 0.05
+    P = rng.standard_normal((seq, d)) * 0.05
+    C = rng.standard_normal((n, k))
+    tok = rng.integers(0, vocab, n).astype(np.int32)
+    pos = (np.arange(n) % seq).astype(np.int32)
+    X = E[tok] + P[pos] + C @ U.T + rng.standard_normal((n, d)) * 0.01
+    G = rng.standard_normal((n, d)) * 0.1
+    if grid:
+        E, P, X = (np.round(a * grid) / grid for a in (E, P, X))
+    st = {name: synth.store(a, dtype) for name, a in
+          dict(U=U, E=E, P=P, C=C, X=X, G=G).items()}
+    f64 = {name: (oracle.decode_bf16(a) if dtype == "bf16" else a.astype(np.float64))
+           for name, a in st.items()}
+    return st, f64, tok, pos
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("d,k,n", [(256, 20, 1), (256, 20, 17), (256, 20, 33), (256, 1, 40),
+                                   (256, 16, 31), (256, 17, 50), (256, 33, 16), (256, 82, 45),
+                                   (256, 128, 20), (384, 130, 19), (200, 20, 37), (96, 5, 64)])
+def test_shapes(dtype, d, k, n):
+    log(f"[shapes] {dtype} d={d} k={k} n={n}")
+    st, o, tok, pos = _small(d, k, n, dtype=dtype, seed=d + k + n)
+    basis = sn.sn_basis_pack(dev(st["U"], dtype))
+    E, P, X, G, Cin = (dev(st[x], dtype) for x in ("E", "P", "X", "G", "C"))
+    t_tok = ids(tok)
+    C = sn.sn_compress(basis, X, tok=t_tok, E=E, P=P, seq_len=9)
+    assert_parity(host(C), oracle.round_to(oracle.compress(o["X"], o["U"], tok, o["E"], o["P"],
+                                                           seq_len=9), dtype), dtype, "compress")
+    Xr = sn.sn_decompress(basis, Cin, tok=t_tok, E=E, P=P, seq_len=9)
+    assert_parity(host(Xr), oracle.round_to(oracle.decompress(o["C"], o["U"], tok, o["E"],
+                                                              o["P"], seq_len=9), dtype),
+                  dtype, "decompress")
+    Cg = sn.sn_grad_compress(basis, G)
+    assert_parity(host(Cg), oracle.round_to(oracle.grad_compress(o["G"], o["U"]), dtype), dtype,
+                  "grad_compress")
+    W = G[: min(n, 64)].T.contiguous() if n >= 1 else None   # d x m
+    Wn = host(W)
+    sn.sn_project_weights(basis, W)
+    assert_parity(host(W).T, oracle.round_to(oracle.project_weights(Wn, o["U"]), dtype).T,
+                  dtype, "project_weights")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_tables_optional_and_explicit_positions(dtype):
+    d, k, n = 256, 24, 70
+    st, o, tok, _ = _small(d, k, n, dtype=dtype, seed=5)
+    rng = np.random.default_rng(6)
+    pos = rng.integers(0, 9, n).astype(np.int32)      # arbitrary (e.g. context-parallel) positions
+    basis = sn.sn_basis_pack(dev(st["U"], dtype))
+    E, P, X, Cin = (dev(st[x], dtype) for x in ("E", "P", "X", "C"))
+    cases = [("E+P explicit pos", dict(tok=ids(tok), E=E, P=P, pos=ids(pos)),
+              dict(tok=tok, E=o["E"], P=o["P"], pos=pos)),
+             ("E only", dict(tok=ids(tok), E=E), dict(tok=tok, E=o["E"])),
+             ("P only default pos", dict(P=P, seq_len=9), dict(P=o["P"], seq_len=9)),
+             ("no tables", {}, {})]
+    for name, gk, ok in cases:
+        C = sn.sn_compress(basis, X, **gk)
+        assert_parity(host(C), oracle.round_to(oracle.compress(o["X"], o["U"], **ok), dtype),
+                      dtype, f"compress {name}")
+        Xr = sn.sn_decompress(basis, Cin, **gk)
+        assert_parity(host(Xr), oracle.round_to(oracle.decompress(o["C"], o["U"], **ok), dtype),
+                      dtype, f"decompress {name}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_strides_and_guard_canaries(dtype):
+    """Row strides larger than the row; nothing is written outside the N x k
+    (resp. N x d) region of a padded output buffer."""
+    d, k, n = 256, 40, 37
+    st, o, tok, _ = _small(d, k, n, dtype=dtype, seed=7)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    basis = sn.sn_basis_pack(dev(st["U"], dtype))
+    E, P = dev(st["E"], dtype), dev(st["P"], dtype)
+    for ldx_pad in (8, 1):
+        Xbig = torch.zeros(n, d + ldx_pad, dtype=tdt, device="cuda")
+        Xbig[:, :d] = dev(st["X"], dtype)
+        X = Xbig[:, :d]
+        Cbig = torch.full((n + 3, k + 5), 7.0, dtype=tdt, device="cuda")
+        C = Cbig[:n, :k]
+        sn.sn_compress(basis, X, tok=ids(tok), E=E, P=P, seq_len=9, out=C)
+        assert_parity(host(C), oracle.round_to(oracle.compress(o["X"], o["U"], tok, o["E"],
+                                                               o["P"], seq_len=9), dtype),
+                      dtype, f"compress ldx=d+{ldx_pad} ldc=k+5")
+        cb = host(Cbig)
+        assert np.all(cb[n:] == 7.0) and np.all(cb[:, k:] == 7.0), "compress wrote outside C"
+        Obig = torch.full((n + 2, d + 16), 7.0, dtype=tdt, device="cuda")
+        Xo = Obig[:n, :d + (0 if ldx_pad == 8 else 0)]
+        Cin = dev(st["C"], dtype)
+        sn.sn_decompress(basis, Cin, tok=ids(tok), E=E, P=P, seq_len=9, out=Xo)
+        assert_parity(host(Xo), oracle.round_to(oracle.decompress(o["C"], o["U"], tok, o["E"],
+                                                                  o["P"], seq_len=9), dtype),
+                      dtype, "decompress into strided output")
+        ob = host(Obig)
+        assert np.all(ob[n:] == 7.0) and np.all(ob[:, d:] == 7.0), "decompress wrote outside X"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_out_of_range_ids_are_clamped_and_flagged(dtype):
+    d, k, n, vocab = 256, 20, 40, 50
+    st, o, tok, _ = _small(d, k, n, vocab=vocab, dtype=dtype, seed=9)
+    bad_tok = tok.copy()
+    bad_tok[3], bad_tok[20] = vocab + 5, -2
+    pos = (np.arange(n) % 9).astype(np.int32)
+    bad_pos = pos.copy()
+    bad_pos[7] = 100
+    basis = sn.sn_basis_pack(dev(st["U"], dtype))
+    E, P, X, Cin = (dev(st[x], dtype) for x in ("E", "P", "X", "C"))
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    C = sn.sn_compress(basis, X, tok=ids(bad_tok), E=E, P=P, pos=ids(bad_pos), err_flag=flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 3
+    ct, cp = np.clip(bad_tok, 0, vocab - 1), np.clip(bad_pos, 0, 8)
+    assert_parity(host(C), oracle.round_to(oracle.compress(o["X"], o["U"], ct, o["E"], o["P"],
+                                                           pos=cp), dtype), dtype,
+                  "compress with clamped ids")
+    flag.zero_()
+    Xr = sn.sn_decompress(basis, Cin, tok=ids(bad_tok), E=E, err_flag=flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 1
+    assert_parity(host(Xr), oracle.round_to(oracle.decompress(o["C"], o["U"], ct, o["E"]),
+                                            dtype), dtype, "decompress with clamped ids")
+
+
+def test_bit_exact_gather_and_subtract():
+    """C = 0 decompresses to exactly E[tok] + P[pos]; X = E[tok] + P[pos]
+    compresses to exactly 0 (values on a grid where every sum is exact)."""
+    d, k, n = 256, 40, 70
+    rng = np.random.default_rng(12)
+    U, _ = np.linalg.qr(rng.standard_normal((d, k)))
+    E = rng.integers(-64, 64, (30, d)) / 64.0
+    P = rng.integers(-64, 64, (9, d)) / 64.0
+    tok = rng.integers(0, 30, n).astype(np.int32)
+    pos = (np.arange(n) % 9).astype(np.int32)
+    for dtype in ("bf16", "f32"):
+        st = {nm: synth.store(a, dtype) for nm, a in dict(U=U, E=E, P=P).items()}
+        basis = sn.sn_basis_pack(dev(st["U"], dtype))
+        Et, Pt = dev(st["E"], dtype), dev(st["P"], dtype)
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        Z = torch.zeros(n, k, dtype=tdt, device="cuda")
+        Xr = sn.sn_decompress(basis, Z, tok=ids(tok), E=Et)
+        assert np.array_equal(host_bits(Xr), host_bits(Et[ids(tok).long()])), "E gather"
+        Xr = sn.sn_decompress(basis, Z, P=Pt, seq_len=9)
+        assert np.array_equal(host_bits(Xr), host_bits(Pt[ids(pos).long()])), "P gather"
+        Xr = sn.sn_decompress(basis, Z, tok=ids(tok), E=Et, P=Pt, seq_len=9)
+        assert np.array_equal(host(Xr), E[tok] + P[pos]), "E + P gather"
+        # compress of X = E[tok] + P[pos]: the embedding rows cancel X exactly.
+        # The matrix-core path sums X U, -P U and -E U in fp32, so C is zero up
+        # to fp32 accumulation error (bounded by d * 2^-24 * sum |terms|);
+        # subtracting a wrong row would leave entries of size ~|x| |u| ~ 1e-1.
+        X = dev(synth.store(E[tok] + P[pos], dtype), dtype)
+        C = host(sn.sn_compress(basis, X, tok=ids(tok), E=Et, P=Pt, seq_len=9))
+        Ud = oracle.decode_bf16(st["U"]) if dtype == "bf16" else st["U"].astype(np.float64)
+        absum = (np.abs(E[tok] + P[pos]) + np.abs(E[tok]) + np.abs(P[pos])) @ np.abs(Ud)
+        assert np.all(np.abs(C) <= d * 2.0 ** -24 * absum), "subtract of the gathered rows"
+        log(f"  bit-exact gather, cancelling subtract ok ({dtype}); max |C| {np.abs(C).max():.3g}")
+
+
+def test_output_rounding_ties_to_even():
+    """Outputs are rounded once, to nearest even: 1 + 2^-8 -> 1, 1 + 3*2^-8 -> 1 + 2^-6."""
+    d, k = 64, 8
+    U = np.eye(d)[:, :k]
+    E = np.ones((2, d))
+    E[1] += 2.0 ** -7
+    P = np.full((1, d), 2.0 ** -8)
+    tok = np.array([0, 1], dtype=np.int32)
+    st = {nm: synth.store(a, "bf16") for nm, a in dict(U=U, E=E, P=P).items()}
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    Z = torch.zeros(2, k, dtype=torch.bfloat16, device="cuda")
+    Xr = host(sn.sn_decompress(basis, Z, tok=ids(tok), E=dev(st["E"], "bf16"),
+                               P=dev(st["P"], "bf16"), seq_len=1))
+    ref = oracle.round_bf16(E[tok] + P[[0, 0]])
+    assert np.array_equal(Xr, ref)
+    assert np.all(Xr[0] == 1.0) and np.all(Xr[1] == 1.0 + 2.0 ** -6)
+
+
+def test_empty_batch_is_a_no_op():
+    st, o, tok, _ = _small(64, 8, 5, dtype="bf16")
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    X = torch.zeros(0, 64, dtype=torch.bfloat16, device="cuda")
+    C = sn.sn_compress(basis, X, tok=ids(np.zeros(0, np.int32)), E=dev(st["E"], "bf16"))
+    assert C.shape == (0, 8)
+    Xr = sn.sn_decompress(basis, torch.zeros(0, 8, dtype=torch.bfloat16, device="cuda"))
+    assert Xr.shape == (0, 64)
+
+
+def test_deterministic_bitwise():
+    w = workload(1)
+    dt = "bf16"
+    basis = sn.sn_basis_pack(dev(w["U"], dt))
+    X, E, P, Cin = dev(w["X"], dt), dev(w["E"], dt), dev(w["P"], dt), dev(synth.store(w["C_true"], dt), dt)
+    tok = ids(w["tok"])
+    c1 = host_bits(sn.sn_compress(basis, X, tok=tok, E=E, P=P, seq_len=w["cfg"].seq))
+    c2 = host_bits(sn.sn_compress(basis, X, tok=tok, E=E, P=P, seq_len=w["cfg"].seq))
+    assert np.array_equal(c1, c2)
+    x1 = host_bits(sn.sn_decompress(basis, Cin, tok=tok, E=E, P=P, seq_len=w["cfg"].seq))
+    x2 = host_bits(sn.sn_decompress(basis, Cin, tok=tok, E=E, P=P, seq_len=w["cfg"].seq))
+    assert np.array_equal(x1, x2)
