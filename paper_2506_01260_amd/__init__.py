@@ -93,9 +93,13 @@ def _torch_dtype(dt: int):
 def _mat(t: torch.Tensor, name: str):
     if not t.is_cuda:
         raise SnError(2, f"{name} must be a device tensor")
-    if t.dim() != 2 or (t.shape[0] > 1 and t.stride(1) != 1) or (t.shape[1] > 1 and t.stride(1) != 1):
-        raise SnError(2, f"{name} must be a 2-D row-major matrix (unit column stride)")
-    return t.data_ptr(), t.shape[0], t.shape[1], max(t.stride(0), t.shape[1])
+    if t.dim() != 2:
+        raise SnError(2, f"{name} must be a 2-D matrix")
+    rows, cols = t.shape
+    if cols > 1 and t.stride(1) != 1:
+        raise SnError(2, f"{name} must be row-major (unit column stride)")
+    ld = t.stride(0) if rows > 1 else cols
+    return t.data_ptr(), rows, cols, max(ld, cols)
 
 
 def _ids(t, name, n):

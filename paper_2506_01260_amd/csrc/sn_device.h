@@ -39,6 +39,46 @@ template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
+// ---- compensated accumulation ----------------------------------------------
+// Dot2 of Ogita, Rump and Oishi ("Accurate sum and dot product", SIAM J. Sci.
+// Comput. 26(6), 2005): Knuth's TwoSum and an FMA-based TwoProduct carry the
+// rounding error of every step in a second float, so a sum or dot product is
+// as accurate as if computed in twice the working precision and then rounded.
+// The _rn intrinsics keep the compiler from contracting or reassociating the
+// error-free transformations.
+struct Dot2 {
+  float s = 0.0f, c = 0.0f;
+  __device__ __forceinline__ void add(float x) {
+    const float t = __fadd_rn(s, x);
+    const float z = __fsub_rn(t, s);
+    const float err = __fadd_rn(__fsub_rn(s, __fsub_rn(t, z)), __fsub_rn(x, z));
+    s = t;
+    c = __fadd_rn(c, err);
+  }
+  __device__ __forceinline__ void add_prod(float a, float b) {
+    const float p = __fmul_rn(a, b);
+    const float e = fmaf(a, b, -p);
+    add(p);
+    c = __fadd_rn(c, e);
+  }
+  __device__ __forceinline__ void merge(float os, float oc) {
+    add(os);
+    c = __fadd_rn(c, oc);
+  }
+  __device__ __forceinline__ float value() const { return __fadd_rn(s, c); }
+};
+
+// Sum a Dot2 over the 64 lanes of a wave (every lane gets the result).
+__device__ __forceinline__ float wave_sum_dot2(Dot2 a) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float os = __shfl_xor(a.s, off, 64);
+    const float oc = __shfl_xor(a.c, off, 64);
+    a.merge(os, oc);
+  }
+  return a.value();
+}
+
 // ---- wave64 reduction -----------------------------------------------------
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

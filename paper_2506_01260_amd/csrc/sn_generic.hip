@@ -2,7 +2,9 @@
 //
 // The generic kernels handle every shape, stride and dtype the ABI accepts:
 // all float32 work, and bf16 work that does not meet the MFMA kernels'
-// alignment / size conditions.  They accumulate in float32 and round once.
+// alignment / size conditions.  Every sum is a compensated (Dot2) float32
+// accumulation, rounded once to the output type, so float32 results stay
+// within a few units in the last place even when the sum cancels.
 #include "sn_device.h"
 #include "sn_internal.h"
 
@@ -147,21 +149,27 @@ __global__ __launch_bounds__(256) void compress_generic_kernel(const float *__re
   if (i >= N) return;
   const Rows<T> rw = resolve_rows<T>(i, ids);
   const T *xr = X + i * ldx;
+  // (X - P - E) U is summed as X U - P U - E U: no rounding of X - P - E.
   for (int64_t j0 = 0; j0 < k; j0 += 8) {
-    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    Dot2 acc[8];
     const int jn = static_cast<int>(k - j0 < 8 ? k - j0 : 8);
     for (int64_t r = lane; r < d; r += 64) {
-      float x = to_f32(xr[r]);
-      if (rw.p) x -= to_f32(rw.p[r]);
-      if (rw.e) x -= to_f32(rw.e[r]);
+      const float x = to_f32(xr[r]);
+      const float p = rw.p ? -to_f32(rw.p[r]) : 0.0f;
+      const float e = rw.e ? -to_f32(rw.e[r]) : 0.0f;
       const float *ur = Uf + r * k + j0;
 #pragma unroll
-      for (int jj = 0; jj < 8; ++jj)
-        if (jj < jn) acc[jj] = fmaf(x, ur[jj], acc[jj]);
+      for (int jj = 0; jj < 8; ++jj) {
+        if (jj < jn) {
+          acc[jj].add_prod(x, ur[jj]);
+          if (rw.p) acc[jj].add_prod(p, ur[jj]);
+          if (rw.e) acc[jj].add_prod(e, ur[jj]);
+        }
+      }
     }
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) {
-      float v = wave_sum(acc[jj]);
+      const float v = wave_sum_dot2(acc[jj]);
       if (lane == 0 && jj < jn) C[i * ldc + j0 + jj] = from_f32<T>(v);
     }
   }
@@ -198,11 +206,11 @@ __global__ __launch_bounds__(256) void decompress_generic_kernel(const float *__
   const Rows<T> rw = resolve_rows<T>(i, ids);
   const T *cr = C + i * ldc;
   const float *ur = Uf + r * k;
-  float acc = 0.0f;
-  for (int64_t j = 0; j < k; ++j) acc = fmaf(to_f32(cr[j]), ur[j], acc);
-  if (rw.p) acc += to_f32(rw.p[r]);
-  if (rw.e) acc += to_f32(rw.e[r]);
-  X[i * ldx + r] = from_f32<T>(acc);
+  Dot2 acc;
+  for (int64_t j = 0; j < k; ++j) acc.add_prod(to_f32(cr[j]), ur[j]);
+  if (rw.p) acc.add(to_f32(rw.p[r]));
+  if (rw.e) acc.add(to_f32(rw.e[r]));
+  X[i * ldx + r] = from_f32<T>(acc.value());
 }
 
 hipError_t launch_decompress_generic(const PackLayout &L, const void *packed, const void *C,
@@ -251,21 +259,19 @@ __global__ __launch_bounds__(256) void project_partial_kernel(const float *__res
   const int64_t s = blockIdx.y;
   const int64_t r0 = s * rows_per_split;
   const int64_t r1 = r0 + rows_per_split < d ? r0 + rows_per_split : d;
-  for (int64_t j0 = 0; j0 < k; j0 += 16) {
-    float acc[16];
-#pragma unroll
-    for (int jj = 0; jj < 16; ++jj) acc[jj] = 0.0f;
-    const int jn = static_cast<int>(k - j0 < 16 ? k - j0 : 16);
+  for (int64_t j0 = 0; j0 < k; j0 += 8) {
+    Dot2 acc[8];
+    const int jn = static_cast<int>(k - j0 < 8 ? k - j0 : 8);
     for (int64_t r = r0; r < r1; ++r) {
       const float w = to_f32(W[r * ldw + c]);
       const float *ur = Uf + r * k + j0;
 #pragma unroll
-      for (int jj = 0; jj < 16; ++jj)
-        if (jj < jn) acc[jj] = fmaf(ur[jj], w, acc[jj]);
+      for (int jj = 0; jj < 8; ++jj)
+        if (jj < jn) acc[jj].add_prod(ur[jj], w);
     }
 #pragma unroll
-    for (int jj = 0; jj < 16; ++jj)
-      if (jj < jn) Tp[(s * k + j0 + jj) * m + c] = acc[jj];
+    for (int jj = 0; jj < 8; ++jj)
+      if (jj < jn) Tp[(s * k + j0 + jj) * m + c] = acc[jj].value();
   }
 }
 
@@ -274,9 +280,9 @@ __global__ __launch_bounds__(256) void project_reduce_kernel(const float *__rest
                                                              float *__restrict__ T) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (idx >= km) return;
-  float acc = 0.0f;
-  for (int64_t s = 0; s < splits; ++s) acc += Tp[s * km + idx];
-  T[idx] = acc;
+  Dot2 acc;
+  for (int64_t s = 0; s < splits; ++s) acc.add(Tp[s * km + idx]);
+  T[idx] = acc.value();
 }
 
 template <typename T>
@@ -289,9 +295,9 @@ __global__ __launch_bounds__(256) void project_expand_kernel(const float *__rest
   const int64_t c = (blockIdx.x - r * cblocks) * 256 + threadIdx.x;
   if (c >= m) return;
   const float *ur = Uf + r * k;
-  float acc = 0.0f;
-  for (int64_t j = 0; j < k; ++j) acc = fmaf(ur[j], Tm[j * m + c], acc);
-  W[r * ldw + c] = from_f32<T>(acc);
+  Dot2 acc;
+  for (int64_t j = 0; j < k; ++j) acc.add_prod(ur[j], Tm[j * m + c]);
+  W[r * ldw + c] = from_f32<T>(acc.value());
 }
 
 hipError_t launch_project_generic(const PackLayout &L, const void *packed, void *W, int64_t m,

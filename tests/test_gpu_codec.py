@@ -147,7 +147,7 @@ def test_golden_fixture_exact(dtype, d_pad):
     log(f"[golden] dtype={dtype} d={d_pad}")
     g, m, ex = _golden(d_pad, dtype)
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
-    t = {n: torch.tensor(a, dtype=tdt, device="cuda") for n, a in m.items()}
+    t = {n: torch.tensor(np.ascontiguousarray(a), dtype=tdt, device="cuda") for n, a in m.items()}
     basis = sn.sn_basis_pack(t["U"])
     tok, pos = ids(np.array(g["tok"])), ids(np.array(g["pos"]))
     C = sn.sn_compress(basis, t["X"], tok=tok, E=t["E"], P=t["P"], pos=pos)
