@@ -132,6 +132,56 @@ int32_t sn_decompress(const void *basis, int64_t d, int64_t k, int32_t dt,
                       void *X, int64_t ldx, int32_t *err_flag, sn_stream stream);
 
 /* ------------------------------------------------------------------------ */
+/* Forward codec against projected tables.                                    */
+/*                                                                            */
+/* Compress is linear in its rows, so (X - P[pos] - T_fixed[tok]) U equals    */
+/* X U - (P U)[pos] - (T_fixed U)[tok] (Sec. 4.3.1 with the product taken     */
+/* term by term).  T_fixed and P are fixed and U changes only at a subspace   */
+/* update (Sec. 4.5), so the projected tables T_fixed U (vocab x k) and P U   */
+/* (n_pos x k) can be built once per basis and every compress then streams X  */
+/* alone instead of also gathering two d-wide rows per token.  The result     */
+/* differs from sn_compress only by rounding: the tables are fp32 and the two */
+/* subtractions are rounded to fp32 after the product.                        */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of the projected-table buffer for rank k, vocab token rows and n_pos
+ * positional rows (0 if invalid; vocab or n_pos may be 0).  Layout: fp32
+ * rows of kp = 16 * ceil(k / 16) elements (columns k..kp-1 are zero);
+ * T_fixed U (vocab rows) at byte offset 0, then P U (n_pos rows) at byte
+ * offset round_up(vocab * kp * 4, 256). */
+size_t sn_embed_projected_bytes(int64_t k, int64_t vocab, int64_t n_pos);
+
+/* sn_embed_project: build the projected tables T_fixed U and P U.
+ *
+ *   basis   packed basis of (d, k, dt)
+ *   E       vocab x d token table (row stride lde >= d); NULL iff vocab == 0
+ *   P       n_pos x d positional table (row stride ldp >= d); NULL iff n_pos == 0
+ *   proj    device buffer of at least sn_embed_projected_bytes(k, vocab, n_pos)
+ *           bytes, 256-byte aligned, fully written; may not overlap an input.
+ * Rebuild after any change of U, E or P; a stale buffer is not detected.
+ * Errors: NULL, SHAPE, DTYPE, ALIGN, ALIAS, WORKSPACE, UNSUPPORTED, HIP. */
+int32_t sn_embed_project(const void *basis, int64_t d, int64_t k, int32_t dt,
+                         const void *E, int64_t vocab, int64_t lde,
+                         const void *P, int64_t n_pos, int64_t ldp,
+                         void *proj, size_t proj_bytes, sn_stream stream);
+
+/* sn_compress_projected:
+ *   C[i, :] = X[i, :] U - (P U)[pos_i, :] - (T_fixed U)[tok[i], :]
+ *
+ *   proj     buffer written by sn_embed_project for the same basis, vocab and
+ *            n_pos (may be NULL when vocab == 0 and n_pos == 0)
+ *   vocab    rows of T_fixed U in proj; 0 = no token term (tok ignored)
+ *   n_pos    rows of P U in proj; 0 = no positional term (pos, seq_len ignored)
+ *   tok, pos, seq_len, X, C, err_flag: as in sn_compress (pos NULL means
+ *            pos_i = i mod seq_len, 1 <= seq_len <= n_pos).
+ * C may not overlap any input.  Errors as sn_compress. */
+int32_t sn_compress_projected(const void *basis, int64_t d, int64_t k, int32_t dt,
+                              const void *X, int64_t N, int64_t ldx,
+                              const int32_t *tok, const int32_t *pos, int64_t seq_len,
+                              const void *proj, int64_t vocab, int64_t n_pos,
+                              void *C, int64_t ldc, int32_t *err_flag, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
 /* Backward codec.                                                            */
 /* ------------------------------------------------------------------------ */
 

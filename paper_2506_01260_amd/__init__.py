@@ -12,6 +12,9 @@ built the first call raises ``RuntimeError``.
     Cg = sn_grad_compress(basis, G)
     Gr = sn_decompress(basis, Cg)
     sn_project_weights(basis, W)                     # in place
+
+    proj = sn_embed_project(basis, E=E, P=P)         # T_fixed U, P U (once per basis)
+    C  = sn_compress_projected(basis, X, proj, tok=tok, seq_len=S)
 """
 from __future__ import annotations
 
@@ -44,6 +47,11 @@ _SIGNATURES = {
     "sn_decompress": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _P, _I64, _I64, _P, _P,
                              _I64, _I64, _I64, _P, _I64, _P, _P]),
     "sn_grad_compress": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _I64, _P]),
+    "sn_embed_projected_bytes": (_SZ, [_I64, _I64, _I64]),
+    "sn_embed_project": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _I64, _I64, _P, _SZ,
+                                _P]),
+    "sn_compress_projected": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _P, _I64, _P,
+                                     _I64, _I64, _P, _I64, _P, _P]),
     "sn_project_weights_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
     "sn_project_weights": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _SZ, _P]),
     "sn_status_string": (ctypes.c_char_p, [_I32]),
@@ -222,6 +230,72 @@ def sn_grad_compress(basis: Basis, G: torch.Tensor, out=None, stream=None) -> to
     cp, _, _, ldc = _mat(out, "out")
     _check(lib().sn_grad_compress(basis.ptr, basis.d, basis.k, basis.dt, gp, N, ldg, cp, ldc,
                                   _stream(stream)))
+    return out
+
+
+class Projected:
+    """Projected tables T_fixed U and P U (fp32, one device buffer) of a basis."""
+
+    def __init__(self, buf: torch.Tensor, basis: Basis, vocab: int, n_pos: int):
+        self.buf, self.basis, self.vocab, self.n_pos = buf, basis, vocab, n_pos
+
+    @property
+    def ptr(self):
+        return self.buf.data_ptr() if self.buf.numel() else None
+
+    def _view(self, off: int, rows: int) -> torch.Tensor:
+        kp = 16 * ((self.basis.k + 15) // 16)
+        return self.buf[off:off + rows * kp * 4].view(torch.float32).view(rows, kp)
+
+    def tables(self):
+        """(T_fixed U, P U) as fp32 views of shape (rows, 16 * ceil(k / 16))."""
+        kp = 16 * ((self.basis.k + 15) // 16)
+        off_pu = (self.vocab * kp * 4 + 255) // 256 * 256
+        return self._view(0, self.vocab), self._view(off_pu, self.n_pos)
+
+
+def sn_embed_projected_bytes(k: int, vocab: int, n_pos: int) -> int:
+    return lib().sn_embed_projected_bytes(k, vocab, n_pos)
+
+
+def sn_embed_project(basis: Basis, E=None, P=None, stream=None) -> Projected:
+    """Build the projected tables T_fixed U and P U once per basis."""
+    _same_d(basis, basis.d, ("E", E), ("P", P))
+    _same_dtype(basis, ("E", E), ("P", P))
+    e_ptr = vocab = lde = 0
+    if E is not None:
+        e_ptr, vocab, _, lde = _mat(E, "E")
+    p_ptr = n_pos = ldp = 0
+    if P is not None:
+        p_ptr, n_pos, _, ldp = _mat(P, "P")
+    nbytes = sn_embed_projected_bytes(basis.k, vocab, n_pos)
+    dev = (E if E is not None else P).device if (E is not None or P is not None) else "cuda"
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    _check(lib().sn_embed_project(basis.ptr, basis.d, basis.k, basis.dt, e_ptr or None, vocab,
+                                  lde, p_ptr or None, n_pos, ldp,
+                                  buf.data_ptr() if nbytes else None, nbytes, _stream(stream)))
+    return Projected(buf, basis, vocab, n_pos)
+
+
+def sn_compress_projected(basis: Basis, X: torch.Tensor, proj: Projected, tok=None, pos=None,
+                          seq_len=None, out=None, err_flag=None, stream=None) -> torch.Tensor:
+    """C = X U - (P U)[pos] - (T_fixed U)[tok] against tables from sn_embed_project."""
+    xp, N, d, ldx = _mat(X, "X")
+    _same_d(basis, d)
+    if proj.basis is not basis:
+        raise SnError(2, "proj was built for another basis")
+    if out is None:
+        out = torch.empty((N, basis.k), dtype=_torch_dtype(basis.dt), device=X.device)
+    _out_shape(out, (N, basis.k), "out")
+    _same_dtype(basis, ("X", X), ("out", out))
+    cp, _, _, ldc = _mat(out, "out")
+    tok_ptr = _ids(tok, "tok", N) if proj.vocab else None
+    pos_ptr = _ids(pos, "pos", N) if proj.n_pos else None
+    _check(lib().sn_compress_projected(basis.ptr, basis.d, basis.k, basis.dt, xp, N, ldx,
+                                       tok_ptr, pos_ptr, int(seq_len or 0), proj.ptr,
+                                       proj.vocab, proj.n_pos, cp, ldc,
+                                       None if err_flag is None else err_flag.data_ptr(),
+                                       _stream(stream)))
     return out
 
 

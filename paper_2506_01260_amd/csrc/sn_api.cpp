@@ -229,6 +229,122 @@ int32_t sn_grad_compress(const void *basis, int64_t d, int64_t k, int32_t dt, co
                      0, Cg, ldc, nullptr, stream);
 }
 
+size_t sn_embed_projected_bytes(int64_t k, int64_t vocab, int64_t n_pos) {
+  if (k < 1 || k > SN_MAX_K || vocab < 0 || vocab >= kMaxDim || n_pos < 0 || n_pos >= kMaxDim)
+    return 0;
+  return sn::proj_layout(k, vocab, n_pos).total;
+}
+
+int32_t sn_embed_project(const void *basis, int64_t d, int64_t k, int32_t dt, const void *E,
+                         int64_t vocab, int64_t lde, const void *P, int64_t n_pos, int64_t ldp,
+                         void *proj, size_t proj_bytes, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (vocab < 0 || vocab >= kMaxDim) return fail(SN_ERR_SHAPE, "vocab out of range");
+  if (n_pos < 0 || n_pos >= kMaxDim) return fail(SN_ERR_SHAPE, "n_pos out of range");
+  if ((vocab > 0) != (E != nullptr)) return fail(SN_ERR_NULL, "E must be given iff vocab > 0");
+  if ((n_pos > 0) != (P != nullptr)) return fail(SN_ERR_NULL, "P must be given iff n_pos > 0");
+  if (E && (lde < d || lde >= kMaxDim)) return fail(SN_ERR_SHAPE, "lde must be >= d");
+  if (P && (ldp < d || ldp >= kMaxDim)) return fail(SN_ERR_SHAPE, "ldp must be >= d");
+  if ((E && !elem_aligned(E, dt)) || (P && !elem_aligned(P, dt)))
+    return fail(SN_ERR_ALIGN, "E or P not aligned to its element size");
+  const sn::ProjLayout PL = sn::proj_layout(k, vocab, n_pos);
+  if (PL.total == 0) return ok();
+  if (!proj) return fail(SN_ERR_NULL, "proj is NULL");
+  if (reinterpret_cast<uintptr_t>(proj) & 255)
+    return fail(SN_ERR_ALIGN, "proj must be 256-byte aligned");
+  if (proj_bytes < PL.total)
+    return fail(SN_ERR_WORKSPACE, "proj has %zu bytes, needs %zu", proj_bytes, PL.total);
+  const size_t es = elem_size(dt);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  Span out;
+  out.lo = reinterpret_cast<uintptr_t>(proj);
+  out.hi = out.lo + PL.total;
+  Span b;
+  b.lo = reinterpret_cast<uintptr_t>(basis);
+  b.hi = b.lo + L.total;
+  if (overlap(out, b) || overlap(out, span(E, vocab, d, lde, es)) ||
+      overlap(out, span(P, n_pos, d, ldp, es)))
+    return fail(SN_ERR_ALIAS, "proj overlaps the basis, E or P");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char *base = static_cast<char *>(proj);
+  const struct {
+    const void *t;
+    int64_t rows, ld;
+    size_t off;
+  } parts[2] = {{E, vocab, lde, PL.off_eu}, {P, n_pos, ldp, PL.off_pu}};
+  for (const auto &pt : parts) {
+    if (pt.rows == 0) continue;
+    float *o = reinterpret_cast<float *>(base + pt.off);
+    hipError_t e = sn::stream_mfma_ok(L, pt.t, pt.ld)
+                       ? sn::launch_table_project_mfma(L, basis, pt.t, pt.rows, pt.ld, o, PL.kp, s)
+                       : sn::launch_table_project_generic(L, basis, pt.t, pt.rows, pt.ld, o,
+                                                          PL.kp, s);
+    if (e != hipSuccess) return hip_status(e, "sn_embed_project launch");
+  }
+  return ok();
+}
+
+int32_t sn_compress_projected(const void *basis, int64_t d, int64_t k, int32_t dt, const void *X,
+                              int64_t N, int64_t ldx, const int32_t *tok, const int32_t *pos,
+                              int64_t seq_len, const void *proj, int64_t vocab, int64_t n_pos,
+                              void *C, int64_t ldc, int32_t *err_flag, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (N < 0 || N >= kMaxDim) return fail(SN_ERR_SHAPE, "N = %lld out of range", (long long)N);
+  if (ldx < d || ldx >= kMaxDim) return fail(SN_ERR_SHAPE, "ldx must be >= d");
+  if (ldc < k || ldc >= kMaxDim) return fail(SN_ERR_SHAPE, "ldc must be >= k");
+  if (vocab < 0 || vocab >= kMaxDim) return fail(SN_ERR_SHAPE, "vocab out of range");
+  if (n_pos < 0 || n_pos >= kMaxDim) return fail(SN_ERR_SHAPE, "n_pos out of range");
+  if ((vocab > 0 || n_pos > 0) && !proj) return fail(SN_ERR_NULL, "proj is NULL");
+  if (proj && (reinterpret_cast<uintptr_t>(proj) & 255))
+    return fail(SN_ERR_ALIGN, "proj must be 256-byte aligned");
+  if (n_pos > 0 && !pos && (seq_len < 1 || seq_len > n_pos))
+    return fail(SN_ERR_SHAPE, "pos is NULL: need 1 <= seq_len <= n_pos (seq_len = %lld)",
+                (long long)seq_len);
+  if ((tok && (reinterpret_cast<uintptr_t>(tok) & 3)) ||
+      (pos && (reinterpret_cast<uintptr_t>(pos) & 3)))
+    return fail(SN_ERR_ALIGN, "tok / pos not 4-byte aligned");
+  if (N == 0) return ok();
+  if (vocab > 0 && !tok) return fail(SN_ERR_NULL, "tok is NULL but vocab > 0");
+  if (!X || !C) return fail(SN_ERR_NULL, "X or C is NULL");
+  if (!elem_aligned(X, dt) || !elem_aligned(C, dt))
+    return fail(SN_ERR_ALIGN, "X or C not aligned to its element size");
+  const size_t es = elem_size(dt);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  const sn::ProjLayout PL = sn::proj_layout(k, vocab, n_pos);
+  const Span out = span(C, N, k, ldc, es);
+  Span b;
+  b.lo = reinterpret_cast<uintptr_t>(basis);
+  b.hi = b.lo + L.total;
+  Span pj;
+  if (proj) {
+    pj.lo = reinterpret_cast<uintptr_t>(proj);
+    pj.hi = pj.lo + PL.total;
+  }
+  if (overlap(out, b) || overlap(out, pj) || overlap(out, span(X, N, d, ldx, es)) ||
+      (vocab > 0 && overlap(out, span(tok, 1, N, N, 4))) ||
+      (n_pos > 0 && pos && overlap(out, span(pos, 1, N, N, 4))))
+    return fail(SN_ERR_ALIAS, "C overlaps an input");
+  const char *pb = static_cast<const char *>(proj);
+  sn::ProjArgs pa{};
+  pa.tok = vocab > 0 ? tok : nullptr;
+  pa.eu = vocab > 0 ? reinterpret_cast<const float *>(pb + PL.off_eu) : nullptr;
+  pa.vocab = vocab;
+  pa.pos = n_pos > 0 ? pos : nullptr;
+  pa.pu = n_pos > 0 ? reinterpret_cast<const float *>(pb + PL.off_pu) : nullptr;
+  pa.n_pos = n_pos;
+  pa.seq_len = (n_pos > 0 && !pos) ? seq_len : 1;
+  pa.kp = PL.kp;
+  pa.err_flag = err_flag;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (sn::stream_mfma_ok(L, X, ldx))
+    return hip_status(sn::launch_compress_projected_mfma(L, basis, X, N, ldx, pa, C, ldc, s),
+                      "sn_compress_projected launch");
+  return hip_status(sn::launch_compress_projected_generic(L, basis, X, N, ldx, pa, C, ldc, s),
+                    "sn_compress_projected launch");
+}
+
 size_t sn_project_weights_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t m) {
   if (!dtype_ok(dt) || d < 1 || d >= kMaxDim || k < 1 || k > d || k > SN_MAX_K || m < 0 ||
       m >= kMaxDim)

@@ -1,0 +1,727 @@
+// The bf16 stage-boundary codec on the gfx950 matrix cores.
+//
+// compress   C[i, :] = (X[i, :] - P[pos_i, :] - E[tok_i, :]) U      (Sec. 4.3.1, Eq. "subtract")
+//            D[j, token] = sum_r U[r, j] * (X - P - E)[token, r], computed as
+//            X U + (-P) U + (-E) U in one set of fp32 accumulators (sign-flipped
+//            bf16 operands), so X - P - E is never rounded: every bf16 product
+//            is exact and every sum is fp32.
+// decompress X[i, :] = C[i, :] U^T + P[pos_i, :] + E[tok_i, :]       (Sec. 4.3.1, recovery)
+//            D[r, token] = sum_j U[r, j] C[token, j], then + P + E in fp32.
+// Without tables these are the gradient codec of Sec. 4.4.
+//
+// Structure (one workgroup = 4 compute waves + 1 producer wave, 64 tokens):
+//
+// * The producer wave copies, for each stage of 128 columns of d, everything
+//   the compute waves need into one of NB LDS buffers with direct-to-LDS
+//   loads: the 64 tokens' X rows (compress), their E and P rows, and the U
+//   fragments of the stage.  Each copy instruction reads 4 rows x 256
+//   contiguous bytes (contiguous row pieces are much cheaper for the memory
+//   pipeline than the 16-rows-x-64-bytes pattern of an MFMA operand), and the
+//   16-byte pieces of row r are stored in the order p ^ (r & 7) so that the
+//   compute waves' operand reads (16 rows, same piece) hit distinct banks.
+// * Compute wave w owns 16 tokens and the whole of d; it reads operands only
+//   from LDS (no global loads in its main loop), so nothing stalls it but the
+//   hand-over barrier.  Decompress stages each output tile in LDS and writes
+//   it back with 256-byte row pieces.
+// * NB-deep buffering: the producer keeps NB-1 stages in flight; one barrier
+//   per stage hands a buffer over.  Workgroups start at different stages
+//   (rotation) so the rows in flight across the chip are not read at the same
+//   column offsets.
+// * Position-major tiles (positions i mod seq_len, batch a multiple of 4): a
+//   16-token tile holds 16/B consecutive positions of B batches, so the tile
+//   needs only 16/B positional rows.
+#include "sn_mfma_common.h"
+
+namespace sn {
+
+namespace {
+
+constexpr int kW = 4;                  // compute waves per workgroup
+constexpr int kThreads = 64 * (kW + 1);
+constexpr int kTokens = 16 * kW;       // tokens per workgroup
+constexpr int kStageCols = 128;        // d-elements per stage
+constexpr int kPieces = 16;            // 16-byte pieces per row per stage
+constexpr int kLdsBytes = 160 * 1024;
+
+// 16-byte LDS slot of piece p of row r in a row tile.
+__device__ __forceinline__ int slot(int r, int p) { return r * kPieces + (p ^ (r & 7)); }
+
+// Token placement of a launch.
+struct Tiling {
+  int64_t N;
+  int64_t seq;      // positions per sequence (position-major tiles only)
+  int bp;           // batches per tile: 1 = token-major, else 4 or 8
+};
+
+// Token of lane n of 16-token tile T (T already clamped to a valid tile);
+// token-major tiles past N repeat token N-1.
+__device__ __forceinline__ int64_t tile_token(const Tiling &tm, int64_t T, int n) {
+  if (tm.bp == 1) {
+    const int64_t t = 16 * T + n;
+    return t < tm.N ? t : tm.N - 1;
+  }
+  const int pg = 16 / tm.bp;
+  const int64_t tpb = tm.seq / pg;
+  const int64_t bg = T / tpb, pt = T - bg * tpb;
+  return (bg * tm.bp + n % tm.bp) * tm.seq + pt * pg + n / tm.bp;
+}
+
+// First position of position-major tile T.
+__device__ __forceinline__ int64_t tile_pos0(const Tiling &tm, int64_t T) {
+  const int pg = 16 / tm.bp;
+  const int64_t tpb = tm.seq / pg;
+  return (T % tpb) * pg;
+}
+
+template <bool PM>
+constexpr int p_rows() { return PM ? 16 : kTokens; }  // positional rows staged per workgroup
+
+// ---------------------------------------------------------------------------
+// Stage buffer geometry (in 16-byte units) for compress / decompress.
+// ---------------------------------------------------------------------------
+template <int KT, bool HE, bool HP, bool PM>
+struct CGeo {
+  static constexpr int x_off = 0;
+  static constexpr int e_off = x_off + kTokens * kPieces;
+  static constexpr int p_off = e_off + (HE ? kTokens * kPieces : 0);
+  static constexpr int u_off = p_off + (HP ? p_rows<PM>() * kPieces : 0);
+  static constexpr int buf_units = u_off + 4 * KT * 64;
+  static constexpr int dma_per_stage = kTokens / 4 + (HE ? kTokens / 4 : 0) +
+                                       (HP ? p_rows<PM>() / 4 : 0) + 4 * KT;
+  static constexpr int nb =
+      (3 * buf_units * 16 <= kLdsBytes && dma_per_stage <= 63) ? 3 : 2;
+  static_assert(nb * buf_units * 16 <= kLdsBytes, "stage buffers exceed LDS");
+};
+
+template <int KS, bool HE, bool HP, bool PM>
+struct DGeo {
+  static constexpr int e_off = 0;
+  static constexpr int p_off = e_off + (HE ? kTokens * kPieces : 0);
+  static constexpr int u_off = p_off + (HP ? p_rows<PM>() * kPieces : 0);
+  static constexpr int buf_units = u_off + 4 * 2 * KS * 64;
+  static constexpr int out_units = kW * 16 * kPieces;  // one output tile per compute wave
+  static constexpr int dma_per_stage =
+      (HE ? kTokens / 4 : 0) + (HP ? p_rows<PM>() / 4 : 0) + 4 * 2 * KS;
+  static constexpr int nb =
+      (3 * buf_units * 16 + out_units * 16 <= kLdsBytes && dma_per_stage <= 63) ? 3 : 2;
+  static_assert(nb * buf_units * 16 + out_units * 16 <= kLdsBytes, "stage buffers exceed LDS");
+};
+
+// ---------------------------------------------------------------------------
+// Producer wave
+// ---------------------------------------------------------------------------
+// Row pointers of the rows this lane copies: row r = 4 i + q of a tile of R
+// rows (q = lane / 16); lane (q, m) copies piece m ^ (r & 7) of row r.
+template <int R>
+struct RowSet {
+  const bf16_t *ptr[R / 4];
+};
+
+template <int R>
+__device__ __forceinline__ void dma_rows(const RowSet<R> &rs, int64_t col, u32x4 *dst, int q,
+                                         int m) {
+#pragma unroll
+  for (int i = 0; i < R / 4; ++i) {
+    const int r = 4 * i + q;
+    lds_dma_16(rs.ptr[i] + col + 8 * (m ^ (r & 7)), dst + i * 64);
+  }
+}
+
+__device__ __forceinline__ void dma_frags(const bf16_t *src, int frags, u32x4 *dst, int lane) {
+  for (int f = 0; f < frags; ++f) lds_dma_16(src + f * 512 + lane * 8, dst + f * 64);
+}
+
+// Pointer to the start of row `row` of a table.
+__device__ __forceinline__ const bf16_t *row_ptr(const void *base, int64_t ld, int64_t row) {
+  return static_cast<const bf16_t *>(base) + row * ld;
+}
+
+// The producer's rows for the workgroup's 64 tokens (tiles T0..T0+3).
+template <bool WITH_X, bool HE, bool HP, bool PM>
+struct ProducerRows {
+  RowSet<kTokens> x, e;
+  RowSet<p_rows<PM>()> p;
+
+  __device__ void init(const Tiling &tm, int64_t T0, int64_t ntiles, const bf16_t *X,
+                       int64_t ldx, const IdArgs &ids, int q) {
+#pragma unroll
+    for (int i = 0; i < kTokens / 4; ++i) {
+      const int r = 4 * i + q;  // token row r = 16 w + n
+      int64_t T = T0 + r / 16;
+      T = T < ntiles ? T : ntiles - 1;
+      const int64_t t = tile_token(tm, T, r % 16);
+      if (WITH_X) x.ptr[i] = X + t * ldx;
+      if (HE) {
+        const int64_t id = clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1);
+        e.ptr[i] = row_ptr(ids.E, ids.lde, id);
+      }
+      if (HP && !PM) {
+        int64_t ps = ids.pos ? static_cast<int64_t>(ids.pos[t]) : t % ids.seq_len;
+        ps = clamp_id(ps, ids.n_pos, ids.err_flag, 2);
+        p.ptr[i] = row_ptr(ids.P, ids.ldp, ps);
+      }
+    }
+    if (HP && PM) {
+      // positional row r = w * pg + rho of the workgroup (rows past 4 pg repeat
+      // the last one so the copy count stays fixed)
+      const int pg = 16 / tm.bp;
+#pragma unroll
+      for (int i = 0; i < p_rows<PM>() / 4; ++i) {
+        int r = 4 * i + q;
+        r = r < kW * pg ? r : kW * pg - 1;
+        int64_t T = T0 + r / pg;
+        T = T < ntiles ? T : ntiles - 1;
+        p.ptr[i] = row_ptr(ids.P, ids.ldp, tile_pos0(tm, T) + r % pg);
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// compress
+// ---------------------------------------------------------------------------
+template <int KT, bool HE, bool HP, bool PM>
+__global__ __launch_bounds__(kThreads) void compress_kernel(const bf16_t *__restrict__ kfrag,
+                                                            int64_t d, int64_t k,
+                                                            const bf16_t *__restrict__ X,
+                                                            int64_t ldx, Tiling tm, IdArgs ids,
+                                                            bf16_t *__restrict__ C, int64_t ldc,
+                                                            int cvec) {
+  using G = CGeo<KT, HE, HP, PM>;
+  constexpr int NB = G::nb;
+  __shared__ u32x4 lds[NB * G::buf_units];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nst = static_cast<int>(d / kStageCols);
+  const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nst));
+  auto phys = [&](int si) { const int v = si + rot; return v >= nst ? v - nst : v; };
+  const int64_t ntiles = (tm.N + 15) / 16;
+  const int64_t T0 = static_cast<int64_t>(blockIdx.x) * kW;
+
+  if (wave == kW) {  // ------------------------------------------------ producer
+    const int q = lane >> 4, m = lane & 15;
+    ProducerRows<true, HE, HP, PM> pr;
+    pr.init(tm, T0, ntiles, X, ldx, ids, q);
+    auto issue = [&](int si) {
+      u32x4 *b = lds + (si % NB) * G::buf_units;
+      const int st = phys(si);
+      const int64_t col = static_cast<int64_t>(st) * kStageCols;
+      dma_rows(pr.x, col, b + G::x_off, q, m);
+      if (HE) dma_rows(pr.e, col, b + G::e_off, q, m);
+      if (HP) dma_rows(pr.p, col, b + G::p_off, q, m);
+      dma_frags(kfrag + static_cast<int64_t>(st) * 4 * KT * 512, 4 * KT, b + G::u_off, lane);
+    };
+#pragma unroll
+    for (int s = 0; s < NB - 1; ++s)
+      if (s < nst) issue(s);
+    for (int s = 0; s < nst; ++s) {
+      // stage s has landed once at most the later in-flight stage is pending
+      if constexpr (NB == 3) {
+        if (s + 1 < nst)
+          wait_vmcnt<G::dma_per_stage>();
+        else
+          wait_vmcnt<0>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      lds_barrier();
+      if (s + NB - 1 < nst) issue(s + NB - 1);
+    }
+    return;
+  }
+
+  // ------------------------------------------------------------ compute waves
+  const int g = lane >> 4, n = lane & 15;
+  const int xrow = 16 * wave + n;
+  const int prow = PM ? wave * (16 / tm.bp) + n / tm.bp : xrow;
+
+  f32x4 acc[KT];
+#pragma unroll
+  for (int t = 0; t < KT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int s = 0; s < nst; ++s) {
+    lds_barrier();  // stage s is in buffer s % NB
+    const u32x4 *b = lds + (s % NB) * G::buf_units;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int pc = 4 * j + g;
+      const u32x4 bx = b[G::x_off + slot(xrow, pc)];
+      u32x4 be, bpv;
+      if (HE) be = neg8(b[G::e_off + slot(xrow, pc)]);
+      if (HP) bpv = neg8(b[G::p_off + slot(prow, pc)]);
+#pragma unroll
+      for (int t = 0; t < KT; ++t) {
+        const u32x4 a = b[G::u_off + (j * KT + t) * 64 + lane];
+        acc[t] = mfma(a, bx, acc[t]);
+        if (HP) acc[t] = mfma(a, bpv, acc[t]);
+        if (HE) acc[t] = mfma(a, be, acc[t]);
+      }
+    }
+  }
+
+  // epilogue: lane (g, n) holds C[token, 16 t + 4 g .. +3]
+  int64_t T = T0 + wave;
+  if (T >= ntiles) return;  // a tile past the end computed a duplicate
+  const int64_t i = 16 * T + n;
+  const int64_t tok = tm.bp == 1 ? i : tile_token(tm, T, n);
+  if (tm.bp == 1 && i >= tm.N) return;
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    const f32x4 v = acc[t];
+    const int64_t j = 16 * t + 4 * g;
+    bf16_t *dst = C + tok * ldc + j;
+    if (cvec && j + 4 <= k) {
+      *reinterpret_cast<u32x2 *>(dst) = u32x2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
+    } else {
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j + e < k) dst[e] = from_f32<bf16_t>(vv[e]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// decompress
+// ---------------------------------------------------------------------------
+template <int KS, bool HE, bool HP, bool PM>
+__global__ __launch_bounds__(kThreads) void decompress_kernel(
+    const bf16_t *__restrict__ rfrag, int64_t d, int64_t k, const bf16_t *__restrict__ C,
+    int64_t ldc, int cvec, Tiling tm, IdArgs ids, bf16_t *__restrict__ X, int64_t ldx) {
+  using G = DGeo<KS, HE, HP, PM>;
+  constexpr int NB = G::nb;
+  constexpr bool NTSTORE = HE || HP;
+  __shared__ u32x4 lds[NB * G::buf_units + G::out_units];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nst = static_cast<int>(d / kStageCols);
+  const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nst));
+  auto phys = [&](int si) { const int v = si + rot; return v >= nst ? v - nst : v; };
+  const int64_t ntiles = (tm.N + 15) / 16;
+  const int64_t T0 = static_cast<int64_t>(blockIdx.x) * kW;
+
+  if (wave == kW) {  // ------------------------------------------------ producer
+    const int q = lane >> 4, m = lane & 15;
+    ProducerRows<false, HE, HP, PM> pr;
+    pr.init(tm, T0, ntiles, nullptr, 0, ids, q);
+    auto issue = [&](int si) {
+      u32x4 *b = lds + (si % NB) * G::buf_units;
+      const int st = phys(si);
+      const int64_t col = static_cast<int64_t>(st) * kStageCols;
+      if (HE) dma_rows(pr.e, col, b + G::e_off, q, m);
+      if (HP) dma_rows(pr.p, col, b + G::p_off, q, m);
+      dma_frags(rfrag + static_cast<int64_t>(st) * 4 * 2 * KS * 512, 4 * 2 * KS, b + G::u_off,
+                lane);
+    };
+#pragma unroll
+    for (int s = 0; s < NB - 1; ++s)
+      if (s < nst) issue(s);
+    for (int s = 0; s < nst; ++s) {
+      if constexpr (NB == 3) {
+        if (s + 1 < nst)
+          wait_vmcnt<G::dma_per_stage>();
+        else
+          wait_vmcnt<0>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      lds_barrier();
+      if (s + NB - 1 < nst) issue(s + NB - 1);
+    }
+    return;
+  }
+
+  // ------------------------------------------------------------ compute waves
+  const int g = lane >> 4, n = lane & 15, q = lane >> 4, m = lane & 15;
+  int64_t T = T0 + wave;
+  T = T < ntiles ? T : ntiles - 1;  // a tile past the end duplicates the last one
+  const int row = 16 * wave + n;
+  const int prow = PM ? wave * (16 / tm.bp) + n / tm.bp : row;
+
+  // B operand: C[token, 32 j + 8 g + e] for this lane's token
+  u32x4 b[KS];
+  {
+    const int64_t tok = tile_token(tm, T, n);
+    const bf16_t *cr = C + tok * ldc;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const int64_t c0 = 32 * j + 8 * g;
+      if (cvec && c0 + 8 <= k) {
+        b[j] = ld16(cr + c0);
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const uint32_t lo = c0 + 2 * e2 < k ? cr[c0 + 2 * e2] : 0u;
+          const uint32_t hi = c0 + 2 * e2 + 1 < k ? cr[c0 + 2 * e2 + 1] : 0u;
+          w[e2] = lo | (hi << 16);
+        }
+        b[j] = u32x4{w[0], w[1], w[2], w[3]};
+      }
+    }
+  }
+  // output rows this lane writes back: row 4 i + q of the wave's tile
+  bf16_t *orow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) orow[i] = X + tile_token(tm, T, 4 * i + q) * ldx;
+  u32x4 *otile = lds + NB * G::buf_units + wave * 16 * kPieces;
+
+  for (int s = 0; s < nst; ++s) {
+    lds_barrier();  // stage s is in buffer s % NB
+    const u32x4 *bu = lds + (s % NB) * G::buf_units;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {  // row group j of the stage: columns 32 j .. 32 j + 31
+      f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int qq = 0; qq < KS; ++qq) {
+        lo = mfma(bu[G::u_off + ((j * 2 + 0) * KS + qq) * 64 + lane], b[qq], lo);
+        hi = mfma(bu[G::u_off + ((j * 2 + 1) * KS + qq) * 64 + lane], b[qq], hi);
+      }
+      // lane holds X[token n, stage col 32 j + 8 g + 0..7]: piece 4 j + g
+      float o[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      const int pc = 4 * j + g;
+      if (HP) {
+        const u32x4 pv = bu[G::p_off + slot(prow, pc)];
+        const uint32_t w[4] = {pv.x, pv.y, pv.z, pv.w};
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          o[2 * e2] += bf_lo(w[e2]);
+          o[2 * e2 + 1] += bf_hi(w[e2]);
+        }
+      }
+      if (HE) {
+        const u32x4 ev = bu[G::e_off + slot(row, pc)];
+        const uint32_t w[4] = {ev.x, ev.y, ev.z, ev.w};
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          o[2 * e2] += bf_lo(w[e2]);
+          o[2 * e2 + 1] += bf_hi(w[e2]);
+        }
+      }
+      otile[slot(n, pc)] = u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
+                                 pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])};
+    }
+    // write the tile back: each store covers 4 rows x 256 contiguous bytes.
+    // Rows of padding tokens repeat token N-1 and carry the same bytes.
+    const int64_t col = static_cast<int64_t>(phys(s)) * kStageCols;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + q;
+      const u32x4 v = otile[slot(r, m ^ (r & 7))];
+      u32x4 *dst = reinterpret_cast<u32x4 *>(orow[i] + col + 8 * (m ^ (r & 7)));
+      if (NTSTORE)
+        __builtin_nontemporal_store(v, dst);
+      else
+        *dst = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// streaming compress: X U with no gathered rows
+// ---------------------------------------------------------------------------
+// Used for the gradient codec (no tables), for the projected-table compress
+// (C = X U - (P U)[pos] - (T_fixed U)[tok], the subtraction done on the k
+// coefficients of each token), and to build those projected tables.  A pure
+// HBM stream of X is fastest when each compute wave issues its own loads:
+// compute wave w owns 16 tokens and keeps D steps of its rows in flight in a
+// register ring; the producer wave copies U chunk by chunk into two LDS
+// buffers (one barrier per chunk).  The ring loads are unconditional (the
+// loads past the end re-read the last step) and pinned in place, so the
+// compiler keeps all D in flight.
+enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2 };
+
+template <int KT>
+constexpr int s_chunk_steps() { return KT <= 4 ? 8 : 4; }
+
+template <int KT, int EPI>
+__global__ __launch_bounds__(kThreads) void stream_compress_kernel(
+    const bf16_t *__restrict__ kfrag, int64_t d, int64_t k, const bf16_t *__restrict__ X,
+    int64_t N, int64_t ldx, ProjArgs pa, void *__restrict__ Cout, int64_t ldc, int cvec) {
+  constexpr int CH = s_chunk_steps<KT>();
+  constexpr int D = CH;  // steps of rows in flight per wave
+  constexpr int CHUNK_FRAGS = CH * KT;
+  __shared__ u32x4 ubuf[2][CHUNK_FRAGS * 64];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int steps = static_cast<int>(d / 32);
+  const int nchunks = (steps + CH - 1) / CH;
+  const int rot = (steps % CH == 0) ? static_cast<int>(blockIdx.x % nchunks) * CH : 0;
+  auto phys = [&](int si) { const int v = si + rot; return v >= steps ? v - steps : v; };
+
+  if (wave == kW) {  // ------------------------------------------------ producer
+    auto copy = [&](int cs) {
+      const int c0 = phys(cs * CH) / CH;
+      const int left = steps - c0 * CH;
+      const int frags = (left < CH ? left : CH) * KT;
+      dma_frags(kfrag + static_cast<int64_t>(c0) * CHUNK_FRAGS * 512, frags, ubuf[cs & 1], lane);
+      wait_vmcnt<0>();
+    };
+    copy(0);
+    lds_barrier();
+    for (int cs = 0; cs < nchunks; ++cs) {
+      if (cs + 1 < nchunks) copy(cs + 1);
+      lds_barrier();
+    }
+    return;
+  }
+
+  const int g = lane >> 4, n = lane & 15;
+  const int64_t tile = static_cast<int64_t>(blockIdx.x) * kW + wave;
+  const int64_t it = 16 * tile + n;
+  const int64_t i = it < N ? it : N - 1;  // padding lanes load token N-1 (not stored)
+  const bf16_t *xr = X + i * ldx + 8 * g;
+
+  f32x4 acc[KT];
+#pragma unroll
+  for (int t = 0; t < KT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto phys_c = [&](int si) { return phys(si < steps ? si : steps - 1); };
+  u32x4 ring[D];
+#pragma unroll
+  for (int r = 0; r < D; ++r) ring[r] = ld16(xr + 32 * phys_c(r));
+
+  const int nfull = steps / CH;
+  for (int cs = 0; cs < nfull; ++cs) {
+    lds_barrier();  // chunk cs is in ubuf[cs & 1]
+    const u32x4 *ub = ubuf[cs & 1];
+#pragma unroll
+    for (int r = 0; r < CH; ++r) {
+      const int si = cs * CH + r;
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[t] = mfma(ub[(r * KT + t) * 64 + lane], ring[r % D], acc[t]);
+      ring[r % D] = ld16(xr + 32 * phys_c(si + D));
+      __builtin_amdgcn_sched_barrier(0);  // keep the refill here (see above)
+    }
+  }
+  if (nfull < nchunks) {  // partial last chunk (no rotation in this case)
+    lds_barrier();
+    const u32x4 *ub = ubuf[nfull & 1];
+#pragma unroll
+    for (int r = 0; r < CH; ++r) {
+      const int si = nfull * CH + r;
+      if (si < steps) {
+#pragma unroll
+        for (int t = 0; t < KT; ++t)
+          acc[t] = mfma(ub[(r * KT + t) * 64 + lane], ring[r % D], acc[t]);
+      }
+    }
+  }
+  lds_barrier();  // matches the producer's last barrier
+
+  if (it >= N) return;
+  if (EPI == kEpiProjected) {
+    // C = X U - (P U)[pos] - (T_fixed U)[tok], in the paper's order
+    if (pa.pu) {
+      int64_t ps = pa.pos ? static_cast<int64_t>(pa.pos[it]) : it % pa.seq_len;
+      ps = clamp_id(ps, pa.n_pos, pa.err_flag, 2);
+      const float *pr = pa.pu + ps * pa.kp + 4 * g;
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[t] -= *reinterpret_cast<const f32x4 *>(pr + 16 * t);
+    }
+    if (pa.eu) {
+      const int64_t tk = clamp_id(pa.tok[it], pa.vocab, pa.err_flag, 1);
+      const float *er = pa.eu + tk * pa.kp + 4 * g;
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[t] -= *reinterpret_cast<const f32x4 *>(er + 16 * t);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    const f32x4 v = acc[t];
+    const int64_t j = 16 * t + 4 * g;
+    if (EPI == kEpiF32) {  // full padded row of the projected table (columns >= k are 0)
+      *reinterpret_cast<f32x4 *>(static_cast<float *>(Cout) + it * ldc + j) = v;
+      continue;
+    }
+    bf16_t *dst = static_cast<bf16_t *>(Cout) + it * ldc + j;
+    if (cvec && j + 4 <= k) {
+      *reinterpret_cast<u32x2 *>(dst) = u32x2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
+    } else {
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j + e < k) dst[e] = from_f32<bf16_t>(vv[e]);
+    }
+  }
+}
+
+template <int KT, int EPI>
+void launch_stream(const bf16_t *kf, const PackLayout &L, const void *X, int64_t N, int64_t ldx,
+                   const ProjArgs &pa, void *C, int64_t ldc, int cvec, hipStream_t s) {
+  dim3 grid(static_cast<unsigned>(ceil_div(ceil_div(N, 16), kW)));
+  stream_compress_kernel<KT, EPI><<<grid, kThreads, 0, s>>>(
+      kf, L.d, L.k, static_cast<const bf16_t *>(X), N, ldx, pa, C, ldc, cvec);
+}
+
+template <int EPI>
+hipError_t launch_stream_kt(const PackLayout &L, const void *packed, const void *X, int64_t N,
+                            int64_t ldx, const ProjArgs &pa, void *C, int64_t ldc, hipStream_t s) {
+  const bf16_t *kf =
+      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_kfrag);
+  const int cvec = ((reinterpret_cast<uintptr_t>(C) & 7) == 0) && (ldc % 4 == 0);
+  switch (L.kt) {
+    case 1: launch_stream<1, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 2: launch_stream<2, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 3: launch_stream<3, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 4: launch_stream<4, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 5: launch_stream<5, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 6: launch_stream<6, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 7: launch_stream<7, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    case 8: launch_stream<8, EPI>(kf, L, X, N, ldx, pa, C, ldc, cvec, s); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+bool tables_ok(const IdArgs &ids) {
+  if (ids.E && (!aligned16(ids.E) || ids.lde % 8 != 0)) return false;
+  if (ids.P && (!aligned16(ids.P) || ids.ldp % 8 != 0)) return false;
+  return true;
+}
+
+// Position-major tiling when the positions are the default i mod seq_len of a
+// row-major [batch, seq_len] batch with batch a multiple of 4 (8 preferred).
+Tiling pick_tiling(int64_t N, const IdArgs &ids) {
+  Tiling tm{N, 1, 1};
+  if (!ids.P || ids.pos || ids.seq_len <= 0 || N % ids.seq_len != 0) return tm;
+  const int64_t batch = N / ids.seq_len;
+  for (int bp : {8, 4}) {
+    const int pg = 16 / bp;
+    // every workgroup holds 4 full tiles: N / 16 must be a multiple of 4
+    if (batch % bp == 0 && ids.seq_len % pg == 0 && (N / 16) % kW == 0) {
+      tm.seq = ids.seq_len;
+      tm.bp = bp;
+      return tm;
+    }
+  }
+  return tm;
+}
+
+template <int KT, bool HE, bool HP, bool PM>
+void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx, const Tiling &tm,
+              const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s) {
+  const int64_t ntiles = (tm.N + 15) / 16;
+  dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
+  compress_kernel<KT, HE, HP, PM><<<grid, kThreads, 0, s>>>(
+      kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, static_cast<bf16_t *>(C), ldc,
+      cvec);
+}
+
+template <int KT>
+void launch_c_kt(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx,
+                 const Tiling &tm, const IdArgs &ids, void *C, int64_t ldc, int cvec,
+                 hipStream_t s) {
+  const bool he = ids.E != nullptr, hp = ids.P != nullptr, pm = tm.bp != 1;
+  if (he && hp && pm)
+    launch_c<KT, true, true, true>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  else if (he && hp)
+    launch_c<KT, true, true, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  else if (he)
+    launch_c<KT, true, false, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  else if (hp && pm)
+    launch_c<KT, false, true, true>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  else if (hp)
+    launch_c<KT, false, true, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  else
+    launch_c<KT, false, false, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+}
+
+template <int KS, bool HE, bool HP, bool PM>
+void launch_d(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc, int cvec,
+              const Tiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+  const int64_t ntiles = (tm.N + 15) / 16;
+  dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
+  decompress_kernel<KS, HE, HP, PM><<<grid, kThreads, 0, s>>>(
+      rf, L.d, L.k, static_cast<const bf16_t *>(C), ldc, cvec, tm, ids, static_cast<bf16_t *>(X),
+      ldx);
+}
+
+template <int KS>
+void launch_d_ks(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc, int cvec,
+                 const Tiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+  const bool he = ids.E != nullptr, hp = ids.P != nullptr, pm = tm.bp != 1;
+  if (he && hp && pm)
+    launch_d<KS, true, true, true>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
+  else if (he && hp)
+    launch_d<KS, true, true, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
+  else if (he)
+    launch_d<KS, true, false, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
+  else if (hp && pm)
+    launch_d<KS, false, true, true>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
+  else if (hp)
+    launch_d<KS, false, true, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
+  else
+    launch_d<KS, false, false, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
+}
+
+}  // namespace
+
+bool compress_mfma_ok(const PackLayout &L, const void *X, int64_t ldx, const IdArgs &ids) {
+  if (!ids.E && !ids.P) return stream_mfma_ok(L, X, ldx);
+  return L.mfma && L.d % kStageCols == 0 && aligned16(X) && ldx % 8 == 0 && tables_ok(ids);
+}
+
+hipError_t launch_compress_mfma(const PackLayout &L, const void *packed, const void *X,
+                                int64_t N, int64_t ldx, const IdArgs &ids, void *C, int64_t ldc,
+                                hipStream_t s) {
+  const bf16_t *kf =
+      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_kfrag);
+  const int cvec = ((reinterpret_cast<uintptr_t>(C) & 7) == 0) && (ldc % 4 == 0);
+  if (!ids.E && !ids.P) return launch_stream_kt<kEpiBf16>(L, packed, X, N, ldx, ProjArgs{}, C, ldc, s);
+  const Tiling tm = pick_tiling(N, ids);
+  switch (L.kt) {
+    case 1: launch_c_kt<1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 2: launch_c_kt<2>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 3: launch_c_kt<3>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 4: launch_c_kt<4>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 5: launch_c_kt<5>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 6: launch_c_kt<6>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 7: launch_c_kt<7>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    case 8: launch_c_kt<8>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs &ids) {
+  return L.mfma && L.d % kStageCols == 0 && aligned16(X) && ldx % 8 == 0 && tables_ok(ids);
+}
+
+hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const void *C,
+                                  int64_t N, int64_t ldc, const IdArgs &ids, void *X,
+                                  int64_t ldx, hipStream_t s) {
+  const bf16_t *rf =
+      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_rfrag);
+  const int cvec = aligned16(C) && (ldc % 8 == 0);
+  const Tiling tm = pick_tiling(N, ids);
+  switch (L.ks) {
+    case 1: launch_d_ks<1>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
+    case 2: launch_d_ks<2>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
+    case 3: launch_d_ks<3>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
+    case 4: launch_d_ks<4>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+bool stream_mfma_ok(const PackLayout &L, const void *X, int64_t ldx) {
+  return L.mfma && aligned16(X) && ldx % 8 == 0;
+}
+
+hipError_t launch_table_project_mfma(const PackLayout &L, const void *packed, const void *T,
+                                     int64_t rows, int64_t ldt, float *out, int64_t kp,
+                                     hipStream_t s) {
+  return launch_stream_kt<kEpiF32>(L, packed, T, rows, ldt, ProjArgs{}, out, kp, s);
+}
+
+hipError_t launch_compress_projected_mfma(const PackLayout &L, const void *packed, const void *X,
+                                          int64_t N, int64_t ldx, const ProjArgs &pa, void *C,
+                                          int64_t ldc, hipStream_t s) {
+  return launch_stream_kt<kEpiProjected>(L, packed, X, N, ldx, pa, C, ldc, s);
+}
+
+}  // namespace sn

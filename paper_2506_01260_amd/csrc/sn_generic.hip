@@ -190,6 +190,95 @@ hipError_t launch_compress_generic(const PackLayout &L, const void *packed, cons
 }
 
 // ---------------------------------------------------------------------------
+// Projected tables and compress against them (one wave per row, as above).
+// TABLE: out[r, j] = (T U)[r, j] as fp32 for j < k, 0 for k <= j < kp.
+// Otherwise: C[i, j] = (X U)[i, j] - (P U)[pos_i, j] - (T_fixed U)[tok_i, j],
+// each subtraction rounded to fp32, then one rounding to the output type.
+// ---------------------------------------------------------------------------
+
+ProjLayout proj_layout(int64_t k, int64_t vocab, int64_t n_pos) {
+  ProjLayout P;
+  P.kp = 16 * ceil_div(k, 16);
+  P.off_eu = 0;
+  P.off_pu = align256(static_cast<size_t>(vocab) * P.kp * sizeof(float));
+  P.total = P.off_pu + align256(static_cast<size_t>(n_pos) * P.kp * sizeof(float));
+  return P;
+}
+
+template <typename T, bool TABLE>
+__global__ __launch_bounds__(256) void project_rows_generic_kernel(
+    const float *__restrict__ Uf, int64_t d, int64_t k, const T *__restrict__ X, int64_t N,
+    int64_t ldx, ProjArgs pa, void *__restrict__ out, int64_t ldo) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (i >= N) return;
+  const T *xr = X + i * ldx;
+  const float *pr = nullptr, *er = nullptr;
+  if (!TABLE) {
+    if (pa.pu) {
+      int64_t p = pa.pos ? static_cast<int64_t>(pa.pos[i]) : i % pa.seq_len;
+      pr = pa.pu + clamp_id(p, pa.n_pos, pa.err_flag, 2) * pa.kp;
+    }
+    if (pa.eu) er = pa.eu + clamp_id(pa.tok[i], pa.vocab, pa.err_flag, 1) * pa.kp;
+  }
+  const int64_t ncols = TABLE ? ldo : k;  // a table row is written out to its padded width
+  for (int64_t j0 = 0; j0 < ncols; j0 += 8) {
+    Dot2 acc[8];
+    const int jn = static_cast<int>(k - j0 < 8 ? (k - j0 > 0 ? k - j0 : 0) : 8);
+    for (int64_t r = lane; r < d && jn > 0; r += 64) {
+      const float x = to_f32(xr[r]);
+      const float *ur = Uf + r * k + j0;
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj)
+        if (jj < jn) acc[jj].add_prod(x, ur[jj]);
+    }
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      float v = wave_sum_dot2(acc[jj]);
+      const int64_t j = j0 + jj;
+      if (lane != 0) continue;
+      if (TABLE) {
+        if (j < ncols) static_cast<float *>(out)[i * ldo + j] = jj < jn ? v : 0.0f;
+      } else if (jj < jn) {
+        if (pr) v = __fsub_rn(v, pr[j]);
+        if (er) v = __fsub_rn(v, er[j]);
+        static_cast<T *>(out)[i * ldo + j] = from_f32<T>(v);
+      }
+    }
+  }
+}
+
+hipError_t launch_table_project_generic(const PackLayout &L, const void *packed, const void *T,
+                                        int64_t rows, int64_t ldt, float *out, int64_t kp,
+                                        hipStream_t s) {
+  const float *Uf = reinterpret_cast<const float *>(static_cast<const char *>(packed) + L.off_f32);
+  dim3 grid(static_cast<unsigned>(ceil_div(rows, 4)));
+  ProjArgs none{};
+  if (L.dt == 0)
+    project_rows_generic_kernel<float, true><<<grid, 256, 0, s>>>(
+        Uf, L.d, L.k, static_cast<const float *>(T), rows, ldt, none, out, kp);
+  else
+    project_rows_generic_kernel<bf16_t, true><<<grid, 256, 0, s>>>(
+        Uf, L.d, L.k, static_cast<const bf16_t *>(T), rows, ldt, none, out, kp);
+  return hipGetLastError();
+}
+
+hipError_t launch_compress_projected_generic(const PackLayout &L, const void *packed,
+                                             const void *X, int64_t N, int64_t ldx,
+                                             const ProjArgs &pa, void *C, int64_t ldc,
+                                             hipStream_t s) {
+  const float *Uf = reinterpret_cast<const float *>(static_cast<const char *>(packed) + L.off_f32);
+  dim3 grid(static_cast<unsigned>(ceil_div(N, 4)));
+  if (L.dt == 0)
+    project_rows_generic_kernel<float, false><<<grid, 256, 0, s>>>(
+        Uf, L.d, L.k, static_cast<const float *>(X), N, ldx, pa, C, ldc);
+  else
+    project_rows_generic_kernel<bf16_t, false><<<grid, 256, 0, s>>>(
+        Uf, L.d, L.k, static_cast<const bf16_t *>(X), N, ldx, pa, C, ldc);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Decompress: one thread per output element; blockIdx.x = token,
 // blockIdx.y = 256-wide slice of d.
 // ---------------------------------------------------------------------------

@@ -75,6 +75,44 @@ hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const
                                   int64_t N, int64_t ldc, const IdArgs &ids, void *X,
                                   int64_t ldx, hipStream_t s);
 
+// Projected tables: T_fixed U (vocab rows) then P U (n_pos rows), fp32, row
+// stride kp = 16 * ceil(k / 16) (columns k..kp-1 are zero), the P U section at
+// a 256-byte aligned offset.
+struct ProjLayout {
+  int64_t kp = 0;
+  size_t off_eu = 0, off_pu = 0, total = 0;
+};
+ProjLayout proj_layout(int64_t k, int64_t vocab, int64_t n_pos);
+
+// Ids and projected rows of a compress against projected tables; eu / pu
+// NULL = no token / positional term.
+struct ProjArgs {
+  const int32_t *tok;
+  const float *eu;
+  int64_t vocab;
+  const int32_t *pos;
+  const float *pu;
+  int64_t n_pos, seq_len;
+  int64_t kp;
+  int32_t *err_flag;
+};
+
+bool stream_mfma_ok(const PackLayout &L, const void *X, int64_t ldx);
+// rows x d table -> rows x kp fp32 (T U), MFMA path
+hipError_t launch_table_project_mfma(const PackLayout &L, const void *packed, const void *T,
+                                     int64_t rows, int64_t ldt, float *out, int64_t kp,
+                                     hipStream_t s);
+hipError_t launch_compress_projected_mfma(const PackLayout &L, const void *packed, const void *X,
+                                          int64_t N, int64_t ldx, const ProjArgs &pa, void *C,
+                                          int64_t ldc, hipStream_t s);
+hipError_t launch_table_project_generic(const PackLayout &L, const void *packed, const void *T,
+                                        int64_t rows, int64_t ldt, float *out, int64_t kp,
+                                        hipStream_t s);
+hipError_t launch_compress_projected_generic(const PackLayout &L, const void *packed,
+                                             const void *X, int64_t N, int64_t ldx,
+                                             const ProjArgs &pa, void *C, int64_t ldc,
+                                             hipStream_t s);
+
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m);
 bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw);
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *W, int64_t m,

@@ -1,0 +1,304 @@
+// Weight confinement W <- U (U^T W) on the gfx950 matrix cores.
+#include "sn_mfma_common.h"
+
+namespace sn {
+
+namespace {
+
+constexpr int kWaves = 4;  // waves per workgroup
+constexpr int kBlock = 64 * kWaves;
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// weight projection W <- U (U^T W), three passes
+// ---------------------------------------------------------------------------
+//  pass 1  Tp[split][c][j] = sum over the split's rows r of U[r, j] W[r, c]
+//          D[j, c] = A[j, r] B[r, c] with A = kfrag.  Lane (g, n) loads the
+//          8-byte pieces W[32 s + 8 g + e, cb + 4 n .. +3], e = 0..7 (16 lanes
+//          cover 128 contiguous bytes of a row), and transposes that 8 x 4
+//          block in registers into four B operands: MFMA instance q serves
+//          columns cb + 4 n + q.  The four waves of a workgroup split the rows
+//          and are summed through LDS in a fixed order.
+//  pass 2  T = sum of the splits (fixed order), split into bf16 hi + lo so the
+//          second contraction sees T to ~16 significant bits.
+//  pass 3  W[r, c] = sum_j U[r, j] T[j, c]; D[c, r] = A[c, j] B[j, r] with
+//          A = T rows (column order chosen so a lane holds 8 consecutive
+//          columns of one row: 16-byte stores) and B = rfrag.
+// W is read only by pass 1 and written only by pass 3 (stream order), so the
+// update is in place.
+
+namespace {
+
+constexpr int kProjCols = 64;  // columns per workgroup in passes 1 and 3
+
+struct ProjPlan {
+  int64_t m_pad;      // m rounded up to kProjCols
+  int kp;             // 16 * kt: fp32 row length of Tp
+  int kp32;           // 32 * ks: bf16 row length of Th / Tl
+  int dsplit;         // row splits in pass 1
+  int64_t rows_per_split;
+  size_t off_tp, off_th, off_tl, total;
+};
+
+ProjPlan proj_plan(int64_t d, int kt, int ks, int64_t m) {
+  ProjPlan P;
+  P.m_pad = ceil_div(m, kProjCols) * kProjCols;
+  P.kp = 16 * kt;
+  P.kp32 = 32 * ks;
+  const int64_t slabs = P.m_pad / kProjCols;
+  int64_t ds = ceil_div(256, slabs);           // aim for >= 256 workgroups
+  const int64_t max_ds = d / 128;               // >= 32 rows per wave
+  if (ds > max_ds) ds = max_ds;
+  if (ds > 8) ds = 8;
+  if (ds < 1) ds = 1;
+  P.rows_per_split = ceil_div(ceil_div(d, ds), 128) * 128;
+  P.dsplit = static_cast<int>(ceil_div(d, P.rows_per_split));
+  size_t off = 0;
+  P.off_tp = off;
+  off = align256(off + static_cast<size_t>(P.dsplit) * P.m_pad * P.kp * sizeof(float));
+  P.off_th = off;
+  off = align256(off + static_cast<size_t>(P.m_pad) * P.kp32 * 2);
+  P.off_tl = off;
+  off = align256(off + static_cast<size_t>(P.m_pad) * P.kp32 * 2);
+  P.total = off;
+  return P;
+}
+
+template <int KT>
+__global__ __launch_bounds__(kBlock) void project_pass1_kernel(
+    const bf16_t *__restrict__ kfrag, int64_t d, const bf16_t *__restrict__ W, int64_t m,
+    int64_t ldw, int64_t rows_per_split, int64_t m_pad, float *__restrict__ Tp) {
+  __shared__ f32x4 red[KT][4][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int g = lane >> 4, n = lane & 15;
+  const int64_t cb = static_cast<int64_t>(blockIdx.x) * kProjCols;
+  const int split = blockIdx.y;
+  const int64_t col = cb + 4 * n;
+  const bool cvalid = col < m;  // m % 8 == 0: all four columns are valid
+
+  const int steps = static_cast<int>(rows_per_split / 32);
+  const int sb = static_cast<int>(split * (rows_per_split / 32));
+  const int send = static_cast<int>(d / 32);
+  int s0 = sb + steps * wave / kWaves;
+  int s1 = sb + steps * (wave + 1) / kWaves;
+  if (s1 > send) s1 = send;
+
+  f32x4 acc[KT][4];
+#pragma unroll
+  for (int t = 0; t < KT; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[t][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const bf16_t *wcol = W + col;
+  const bf16_t *ufrag = kfrag + lane * 8;
+  for (int s = s0; s < s1; ++s) {
+    u32x2 v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int64_t r = 32 * static_cast<int64_t>(s) + 8 * g + e;
+      v[e] = cvalid ? *reinterpret_cast<const u32x2 *>(wcol + r * ldw) : u32x2{0u, 0u};
+    }
+    u32x4 b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const u32x2 lo = v[2 * i], hi = v[2 * i + 1];
+      b[0][i] = (lo.x & 0xFFFFu) | (hi.x << 16);
+      b[1][i] = (lo.x >> 16) | (hi.x & 0xFFFF0000u);
+      b[2][i] = (lo.y & 0xFFFFu) | (hi.y << 16);
+      b[3][i] = (lo.y >> 16) | (hi.y & 0xFFFF0000u);
+    }
+#pragma unroll
+    for (int t = 0; t < KT; ++t) {
+      const u32x4 a = ld16(ufrag + (static_cast<int64_t>(s) * KT + t) * 512);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[t][q] = mfma(a, b[q], acc[t][q]);
+    }
+  }
+
+  // fixed-order reduction: acc0 + (acc1 + (acc2 + acc3))
+  for (int w = kWaves - 1; w >= 1; --w) {
+    if (wave == w) {
+#pragma unroll
+      for (int t = 0; t < KT; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          f32x4 v = acc[t][q];
+          if (w < kWaves - 1) v += red[t][q][lane];
+          red[t][q][lane] = v;
+        }
+    }
+    __syncthreads();
+  }
+  if (wave == 0 && cvalid) {
+    // lane holds T[16 t + 4 g + i][col + q]
+#pragma unroll
+    for (int t = 0; t < KT; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 v = acc[t][q] + red[t][q][lane];
+        float *dst = Tp + ((static_cast<int64_t>(split) * m_pad + col + q) * (16 * KT)) + 16 * t + 4 * g;
+        *reinterpret_cast<f32x4 *>(dst) = v;
+      }
+  }
+}
+
+// pass 2: one thread per (column c, j): sum the splits, split into hi / lo.
+__global__ __launch_bounds__(256) void project_pass2_kernel(const float *__restrict__ Tp,
+                                                            int dsplit, int64_t m, int64_t m_pad,
+                                                            int kp, int kp32,
+                                                            bf16_t *__restrict__ Th,
+                                                            bf16_t *__restrict__ Tl) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= m_pad * kp32) return;
+  const int64_t c = idx / kp32;
+  const int j = static_cast<int>(idx - c * kp32);
+  float v = 0.0f;
+  if (c < m && j < kp) {
+    Dot2 acc;
+    for (int sp = 0; sp < dsplit; ++sp) acc.add(Tp[(sp * m_pad + c) * kp + j]);
+    v = acc.value();
+  }
+  const bf16_t hi = from_f32<bf16_t>(v);
+  const bf16_t lo = from_f32<bf16_t>(v - to_f32(hi));
+  Th[idx] = hi;
+  Tl[idx] = lo;
+}
+
+template <int KS>
+__global__ __launch_bounds__(kBlock) void project_pass3_kernel(
+    const bf16_t *__restrict__ rfrag, int64_t d, const bf16_t *__restrict__ Th,
+    const bf16_t *__restrict__ Tl, bf16_t *__restrict__ W, int64_t m, int64_t ldw,
+    int64_t rows_per_block) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int g = lane >> 4, n = lane & 15;
+  const int64_t cb = static_cast<int64_t>(blockIdx.x) * kProjCols;
+
+  // A operands: M-tile a covers columns cb + 32 (a / 2) + 8 (mm / 4) + 4 (a % 2) + mm % 4
+  u32x4 ah[4][KS], al[4][KS];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int64_t crow = cb + 32 * (a >> 1) + 8 * (n >> 2) + 4 * (a & 1) + (n & 3);
+#pragma unroll
+    for (int q = 0; q < KS; ++q) {
+      ah[a][q] = ld16(Th + crow * (32 * KS) + 32 * q + 8 * g);
+      al[a][q] = ld16(Tl + crow * (32 * KS) + 32 * q + 8 * g);
+    }
+  }
+
+  const int64_t r_begin = static_cast<int64_t>(blockIdx.y) * rows_per_block;
+  const int gb = static_cast<int>(r_begin / 32);
+  const int gcount = static_cast<int>(rows_per_block / 32);
+  int p0 = gb + gcount * wave / kWaves;
+  int p1 = gb + gcount * (wave + 1) / kWaves;
+  const int pend = static_cast<int>(d / 32);
+  if (p1 > pend) p1 = pend;
+  const bf16_t *ufrag = rfrag + lane * 8;
+
+  for (int p = p0; p < p1; ++p) {
+    u32x4 b[2][KS];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int q = 0; q < KS; ++q)
+        b[h][q] = ld16(ufrag + ((static_cast<int64_t>(p) * 2 + h) * KS + q) * 512);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t r = 32 * static_cast<int64_t>(p) + 8 * (n >> 2) + 4 * h + (n & 3);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        f32x4 o[2];
+#pragma unroll
+        for (int a2 = 0; a2 < 2; ++a2) {
+          const int a = 2 * half + a2;
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int q = 0; q < KS; ++q) {
+            acc = mfma(ah[a][q], b[h][q], acc);
+            acc = mfma(al[a][q], b[h][q], acc);
+          }
+          o[a2] = acc;
+        }
+        // lane holds W[r, cb + 32 half + 8 g + 0..7]
+        const int64_t c0 = cb + 32 * half + 8 * g;
+        if (c0 < m) {
+          *reinterpret_cast<u32x4 *>(W + r * ldw + c0) =
+              u32x4{pack_bf16x2(o[0].x, o[0].y), pack_bf16x2(o[0].z, o[0].w),
+                    pack_bf16x2(o[1].x, o[1].y), pack_bf16x2(o[1].z, o[1].w)};
+        }
+      }
+    }
+  }
+}
+
+template <int KT>
+void launch_p1(const ProjPlan &P, const bf16_t *kf, int64_t d, const bf16_t *W, int64_t m,
+               int64_t ldw, float *Tp, hipStream_t s) {
+  dim3 grid(static_cast<unsigned>(P.m_pad / kProjCols), static_cast<unsigned>(P.dsplit));
+  project_pass1_kernel<KT><<<grid, kBlock, 0, s>>>(kf, d, W, m, ldw, P.rows_per_split, P.m_pad,
+                                                   Tp);
+}
+
+template <int KS>
+void launch_p3(const ProjPlan &P, const bf16_t *rf, int64_t d, const bf16_t *Th,
+               const bf16_t *Tl, bf16_t *W, int64_t m, int64_t ldw, hipStream_t s) {
+  const int64_t slabs = P.m_pad / kProjCols;
+  int64_t rsplit = ceil_div(512, slabs);
+  const int64_t max_rs = d / 128;
+  if (rsplit > max_rs) rsplit = max_rs;
+  if (rsplit < 1) rsplit = 1;
+  const int64_t rows = ceil_div(ceil_div(d, rsplit), 128) * 128;
+  rsplit = ceil_div(d, rows);
+  dim3 grid(static_cast<unsigned>(slabs), static_cast<unsigned>(rsplit));
+  project_pass3_kernel<KS><<<grid, kBlock, 0, s>>>(rf, d, Th, Tl, W, m, ldw, rows);
+}
+
+}  // namespace
+
+size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m) {
+  const int kt = static_cast<int>(ceil_div(k, 16)), ks = static_cast<int>(ceil_div(k, 32));
+  return proj_plan(d, kt, ks, m).total;
+}
+
+bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw) {
+  return L.mfma && aligned16(W) && ldw % 8 == 0 && m % 8 == 0 && L.d % 128 == 0;
+}
+
+hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv, int64_t m,
+                               int64_t ldw, void *ws, hipStream_t s) {
+  const ProjPlan P = proj_plan(L.d, L.kt, L.ks, m);
+  const char *base = static_cast<const char *>(packed);
+  const bf16_t *kf = reinterpret_cast<const bf16_t *>(base + L.off_kfrag);
+  const bf16_t *rf = reinterpret_cast<const bf16_t *>(base + L.off_rfrag);
+  char *w = static_cast<char *>(ws);
+  float *Tp = reinterpret_cast<float *>(w + P.off_tp);
+  bf16_t *Th = reinterpret_cast<bf16_t *>(w + P.off_th);
+  bf16_t *Tl = reinterpret_cast<bf16_t *>(w + P.off_tl);
+  bf16_t *W = static_cast<bf16_t *>(Wv);
+  switch (L.kt) {
+    case 1: launch_p1<1>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 2: launch_p1<2>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 3: launch_p1<3>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 4: launch_p1<4>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 5: launch_p1<5>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 6: launch_p1<6>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 7: launch_p1<7>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 8: launch_p1<8>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    default: return hipErrorNotSupported;
+  }
+  const int64_t n2 = P.m_pad * P.kp32;
+  project_pass2_kernel<<<dim3(static_cast<unsigned>(ceil_div(n2, 256))), 256, 0, s>>>(
+      Tp, P.dsplit, m, P.m_pad, P.kp, P.kp32, Th, Tl);
+  switch (L.ks) {
+    case 1: launch_p3<1>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
+    case 2: launch_p3<2>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
+    case 3: launch_p3<3>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
+    case 4: launch_p3<4>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sn

@@ -117,3 +117,47 @@ def test_binding_rejects_host_tensors():
     U = torch.zeros(64, 8, dtype=torch.bfloat16)
     with pytest.raises(sn.SnError):
         sn.sn_basis_pack(U)
+
+
+def test_projected_tables_validation():
+    L = sn.lib()
+    # layout: fp32 rows padded to 16 * ceil(k / 16); P U section 256-byte aligned
+    assert L.sn_embed_projected_bytes(40, 10, 4) == 2048 + 768     # kp = 48
+    assert L.sn_embed_projected_bytes(16, 3, 0) == 256
+    assert L.sn_embed_projected_bytes(40, 0, 0) == 0
+    assert L.sn_embed_projected_bytes(0, 10, 4) == 0
+    assert L.sn_embed_projected_bytes(40, -1, 4) == 0
+    need = L.sn_embed_projected_bytes(8, 10, 4)
+    E, P, out = FAKE + (1 << 20), FAKE + (2 << 20), FAKE + (8 << 20)
+    ok = dict(E=E, vocab=10, lde=256, P=P, n_pos=4, ldp=256, out=out, nbytes=need)
+
+    def embed(**over):
+        a = dict(ok)
+        a.update(over)
+        return L.sn_embed_project(FAKE, 256, 8, 1, a["E"], a["vocab"], a["lde"], a["P"],
+                                  a["n_pos"], a["ldp"], a["out"], a["nbytes"], None)
+    assert embed(E=None) == 1                     # vocab > 0 without E
+    assert embed(P=None) == 1
+    assert embed(vocab=0) == 1                    # E given with vocab == 0
+    assert embed(lde=100) == 2
+    assert embed(nbytes=need - 1) == 9
+    assert embed(out=out + 64) == 4
+    assert embed(out=E) == 5                      # overlaps E
+    assert embed(out=FAKE) == 5                   # overlaps the basis
+    assert embed(E=None, vocab=0, P=None, n_pos=0, out=None, nbytes=0) == 0
+
+    def comp(**over):
+        a = dict(X=FAKE + (3 << 20), N=16, ldx=256, tok=FAKE + (4 << 20), pos=None, seq_len=4,
+                 proj=out, vocab=10, n_pos=4, C=FAKE + (5 << 20), ldc=8)
+        a.update(over)
+        return L.sn_compress_projected(FAKE, 256, 8, 1, a["X"], a["N"], a["ldx"], a["tok"],
+                                       a["pos"], a["seq_len"], a["proj"], a["vocab"],
+                                       a["n_pos"], a["C"], a["ldc"], None, None)
+    assert comp(proj=None) == 1
+    assert comp(proj=out + 16) == 4
+    assert comp(tok=None) == 1
+    assert comp(seq_len=0) == 2 and comp(seq_len=5) == 2
+    assert comp(ldc=7) == 2 and comp(ldx=255) == 2
+    assert comp(C=out) == 5                       # C overlaps the tables
+    assert comp(C=FAKE + (3 << 20)) == 5          # C overlaps X
+    assert comp(N=0, X=None, C=None) == 0
