@@ -93,20 +93,6 @@ struct CGeo {
   static_assert(nb * buf_units * 16 <= kLdsBytes, "stage buffers exceed LDS");
 };
 
-template <int KS, bool HE, bool HP, bool PM>
-struct DGeo {
-  static constexpr int e_off = 0;
-  static constexpr int p_off = e_off + (HE ? kTokens * kPieces : 0);
-  static constexpr int u_off = p_off + (HP ? p_rows<PM>() * kPieces : 0);
-  static constexpr int buf_units = u_off + 4 * 2 * KS * 64;
-  static constexpr int out_units = kW * 16 * kPieces;  // one output tile per compute wave
-  static constexpr int dma_per_stage =
-      (HE ? kTokens / 4 : 0) + (HP ? p_rows<PM>() / 4 : 0) + 4 * 2 * KS;
-  static constexpr int nb =
-      (3 * buf_units * 16 + out_units * 16 <= kLdsBytes && dma_per_stage <= 63) ? 3 : 2;
-  static_assert(nb * buf_units * 16 + out_units * 16 <= kLdsBytes, "stage buffers exceed LDS");
-};
-
 // ---------------------------------------------------------------------------
 // Producer wave
 // ---------------------------------------------------------------------------
@@ -278,143 +264,6 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const bf16_t *__rest
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         if (j + e < k) dst[e] = from_f32<bf16_t>(vv[e]);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// decompress
-// ---------------------------------------------------------------------------
-template <int KS, bool HE, bool HP, bool PM>
-__global__ __launch_bounds__(kThreads) void decompress_kernel(
-    const bf16_t *__restrict__ rfrag, int64_t d, int64_t k, const bf16_t *__restrict__ C,
-    int64_t ldc, int cvec, Tiling tm, IdArgs ids, bf16_t *__restrict__ X, int64_t ldx) {
-  using G = DGeo<KS, HE, HP, PM>;
-  constexpr int NB = G::nb;
-  constexpr bool NTSTORE = HE || HP;
-  __shared__ u32x4 lds[NB * G::buf_units + G::out_units];
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nst = static_cast<int>(d / kStageCols);
-  const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nst));
-  auto phys = [&](int si) { const int v = si + rot; return v >= nst ? v - nst : v; };
-  const int64_t ntiles = (tm.N + 15) / 16;
-  const int64_t T0 = static_cast<int64_t>(blockIdx.x) * kW;
-
-  if (wave == kW) {  // ------------------------------------------------ producer
-    const int q = lane >> 4, m = lane & 15;
-    ProducerRows<false, HE, HP, PM> pr;
-    pr.init(tm, T0, ntiles, nullptr, 0, ids, q);
-    auto issue = [&](int si) {
-      u32x4 *b = lds + (si % NB) * G::buf_units;
-      const int st = phys(si);
-      const int64_t col = static_cast<int64_t>(st) * kStageCols;
-      if (HE) dma_rows(pr.e, col, b + G::e_off, q, m);
-      if (HP) dma_rows(pr.p, col, b + G::p_off, q, m);
-      dma_frags(rfrag + static_cast<int64_t>(st) * 4 * 2 * KS * 512, 4 * 2 * KS, b + G::u_off,
-                lane);
-    };
-#pragma unroll
-    for (int s = 0; s < NB - 1; ++s)
-      if (s < nst) issue(s);
-    for (int s = 0; s < nst; ++s) {
-      if constexpr (NB == 3) {
-        if (s + 1 < nst)
-          wait_vmcnt<G::dma_per_stage>();
-        else
-          wait_vmcnt<0>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      lds_barrier();
-      if (s + NB - 1 < nst) issue(s + NB - 1);
-    }
-    return;
-  }
-
-  // ------------------------------------------------------------ compute waves
-  const int g = lane >> 4, n = lane & 15, q = lane >> 4, m = lane & 15;
-  int64_t T = T0 + wave;
-  T = T < ntiles ? T : ntiles - 1;  // a tile past the end duplicates the last one
-  const int row = 16 * wave + n;
-  const int prow = PM ? wave * (16 / tm.bp) + n / tm.bp : row;
-
-  // B operand: C[token, 32 j + 8 g + e] for this lane's token
-  u32x4 b[KS];
-  {
-    const int64_t tok = tile_token(tm, T, n);
-    const bf16_t *cr = C + tok * ldc;
-#pragma unroll
-    for (int j = 0; j < KS; ++j) {
-      const int64_t c0 = 32 * j + 8 * g;
-      if (cvec && c0 + 8 <= k) {
-        b[j] = ld16(cr + c0);
-      } else {
-        uint32_t w[4];
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          const uint32_t lo = c0 + 2 * e2 < k ? cr[c0 + 2 * e2] : 0u;
-          const uint32_t hi = c0 + 2 * e2 + 1 < k ? cr[c0 + 2 * e2 + 1] : 0u;
-          w[e2] = lo | (hi << 16);
-        }
-        b[j] = u32x4{w[0], w[1], w[2], w[3]};
-      }
-    }
-  }
-  // output rows this lane writes back: row 4 i + q of the wave's tile
-  bf16_t *orow[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) orow[i] = X + tile_token(tm, T, 4 * i + q) * ldx;
-  u32x4 *otile = lds + NB * G::buf_units + wave * 16 * kPieces;
-
-  for (int s = 0; s < nst; ++s) {
-    lds_barrier();  // stage s is in buffer s % NB
-    const u32x4 *bu = lds + (s % NB) * G::buf_units;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {  // row group j of the stage: columns 32 j .. 32 j + 31
-      f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int qq = 0; qq < KS; ++qq) {
-        lo = mfma(bu[G::u_off + ((j * 2 + 0) * KS + qq) * 64 + lane], b[qq], lo);
-        hi = mfma(bu[G::u_off + ((j * 2 + 1) * KS + qq) * 64 + lane], b[qq], hi);
-      }
-      // lane holds X[token n, stage col 32 j + 8 g + 0..7]: piece 4 j + g
-      float o[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-      const int pc = 4 * j + g;
-      if (HP) {
-        const u32x4 pv = bu[G::p_off + slot(prow, pc)];
-        const uint32_t w[4] = {pv.x, pv.y, pv.z, pv.w};
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          o[2 * e2] += bf_lo(w[e2]);
-          o[2 * e2 + 1] += bf_hi(w[e2]);
-        }
-      }
-      if (HE) {
-        const u32x4 ev = bu[G::e_off + slot(row, pc)];
-        const uint32_t w[4] = {ev.x, ev.y, ev.z, ev.w};
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          o[2 * e2] += bf_lo(w[e2]);
-          o[2 * e2 + 1] += bf_hi(w[e2]);
-        }
-      }
-      otile[slot(n, pc)] = u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
-                                 pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])};
-    }
-    // write the tile back: each store covers 4 rows x 256 contiguous bytes.
-    // Rows of padding tokens repeat token N-1 and carry the same bytes.
-    const int64_t col = static_cast<int64_t>(phys(s)) * kStageCols;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 4 * i + q;
-      const u32x4 v = otile[slot(r, m ^ (r & 7))];
-      u32x4 *dst = reinterpret_cast<u32x4 *>(orow[i] + col + 8 * (m ^ (r & 7)));
-      if (NTSTORE)
-        __builtin_nontemporal_store(v, dst);
-      else
-        *dst = v;
     }
   }
 }
@@ -630,34 +479,6 @@ void launch_c_kt(const bf16_t *kf, const PackLayout &L, const void *X, int64_t l
     launch_c<KT, false, false, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
 }
 
-template <int KS, bool HE, bool HP, bool PM>
-void launch_d(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc, int cvec,
-              const Tiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
-  const int64_t ntiles = (tm.N + 15) / 16;
-  dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
-  decompress_kernel<KS, HE, HP, PM><<<grid, kThreads, 0, s>>>(
-      rf, L.d, L.k, static_cast<const bf16_t *>(C), ldc, cvec, tm, ids, static_cast<bf16_t *>(X),
-      ldx);
-}
-
-template <int KS>
-void launch_d_ks(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc, int cvec,
-                 const Tiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
-  const bool he = ids.E != nullptr, hp = ids.P != nullptr, pm = tm.bp != 1;
-  if (he && hp && pm)
-    launch_d<KS, true, true, true>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
-  else if (he && hp)
-    launch_d<KS, true, true, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
-  else if (he)
-    launch_d<KS, true, false, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
-  else if (hp && pm)
-    launch_d<KS, false, true, true>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
-  else if (hp)
-    launch_d<KS, false, true, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
-  else
-    launch_d<KS, false, false, false>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s);
-}
-
 }  // namespace
 
 bool compress_mfma_ok(const PackLayout &L, const void *X, int64_t ldx, const IdArgs &ids) {
@@ -682,27 +503,6 @@ hipError_t launch_compress_mfma(const PackLayout &L, const void *packed, const v
     case 6: launch_c_kt<6>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
     case 7: launch_c_kt<7>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
     case 8: launch_c_kt<8>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
-    default: return hipErrorNotSupported;
-  }
-  return hipGetLastError();
-}
-
-bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs &ids) {
-  return L.mfma && L.d % kStageCols == 0 && aligned16(X) && ldx % 8 == 0 && tables_ok(ids);
-}
-
-hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const void *C,
-                                  int64_t N, int64_t ldc, const IdArgs &ids, void *X,
-                                  int64_t ldx, hipStream_t s) {
-  const bf16_t *rf =
-      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_rfrag);
-  const int cvec = aligned16(C) && (ldc % 8 == 0);
-  const Tiling tm = pick_tiling(N, ids);
-  switch (L.ks) {
-    case 1: launch_d_ks<1>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
-    case 2: launch_d_ks<2>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
-    case 3: launch_d_ks<3>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
-    case 4: launch_d_ks<4>(rf, L, C, ldc, cvec, tm, ids, X, ldx, s); break;
     default: return hipErrorNotSupported;
   }
   return hipGetLastError();

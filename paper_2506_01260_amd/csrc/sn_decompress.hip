@@ -1,0 +1,382 @@
+// Matrix-core decompress: X[i, :] = C[i, :] U^T + P[pos_i, :] + T_fixed[tok[i], :]
+// (Sec. 4.3.1; with no tables, the gradient recovery Cg U^T of Sec. 4.4).
+//
+// Work split: a workgroup owns one 256-column block of X and a run of
+// 16-token tiles; consecutive workgroups take consecutive token runs of the
+// same column block.  The block's slice of U (rfrag layout, 8 row groups of
+// 32 columns) is copied into LDS once and stays there, so the main loop has
+// no barriers: every wave walks its own tiles.
+//
+// Per tile and 128-column chunk a wave
+//  1. runs 4 row groups x 2 x ceil(k/32) MFMAs (A = U fragment from LDS,
+//     B = the tile's coefficients); lane (g, n) gets 8 consecutive columns
+//     of token n in fp32;
+//  2. passes the fp32 tile through a wave-private LDS buffer to the row
+//     layout in which every memory instruction covers 4 rows x 256
+//     contiguous bytes (lane (q, m): rows 4 i + q, columns 8 m .. 8 m + 7);
+//  3. adds the P and T_fixed values of those columns, loaded one chunk ahead
+//     in the same row layout, rounds once to bf16 and stores 16 bytes.
+// Contiguous 256-byte row pieces are the cheapest pattern for both the
+// gathers and the stores; the MFMA operand layout (16 rows x 64 bytes per
+// instruction) is markedly slower for both.
+#include "sn_mfma_common.h"
+
+namespace sn {
+namespace {
+
+constexpr int kDW = 4;              // waves per workgroup
+constexpr int kDThreads = 64 * kDW;
+constexpr int kPG = 8;              // 32-column row groups per column block (256 columns)
+constexpr int kDCols = 32 * kPG;    // columns per block
+constexpr int kNC = kPG / 4;        // 128-column chunks per block
+constexpr int kMaxWaveTiles = 16;   // tiles per wave (ids staged in LDS)
+
+struct DTiling {
+  int N;           // tokens (< 2^31)
+  int seq, batch;  // position-major tile order when batch > 0
+};
+
+// First token of tile T and, in position-major order, its first position:
+// the batch index varies fastest, so neighbouring tiles share positional rows.
+__device__ __forceinline__ int dtile_token0(const DTiling &tm, unsigned T) {
+  if (tm.batch > 0) return static_cast<int>((T % tm.batch) * tm.seq + (T / tm.batch) * 16);
+  return static_cast<int>(16 * T);
+}
+__device__ __forceinline__ int dtile_pos0(const DTiling &tm, unsigned T) {
+  return static_cast<int>((T / tm.batch) * 16);
+}
+
+// Out-of-range id: clamp it into the table and remember the flag bit.
+__device__ __forceinline__ int64_t clamp_flag(int64_t id, int64_t rows, int bit, int &bad) {
+  bad |= (id < 0 || id >= rows) ? bit : 0;
+  return id < 0 ? 0 : (id >= rows ? rows - 1 : id);
+}
+
+// 16-byte slot of (row r, 4-float unit u) in a wave's 16 x 128 fp32 tile.
+// Units 2m and 2m+1 (the 8 columns lane m reads back) are split into the two
+// halves of the row and the position is XORed with the row, so both the
+// MFMA-layout writes (16 rows, one unit) and the row-layout reads (one row,
+// 16 units) touch 16 distinct bank groups.
+__device__ __forceinline__ int ot_slot(int r, int u) {
+  return r * 32 + (((u >> 1) | ((u & 1) << 4)) ^ (r & 15));
+}
+
+// Per-tile state of a lane: the MFMA B operand (coefficients of token n) and,
+// for its 4 rows 4 i + q of the row layout, the token, T_fixed row and P row
+// (row indices, not pointers: 32-bit registers).
+template <int KS>
+struct DTile {
+  u32x4 b[KS];
+  int er[4], pr[4], xr[4];
+};
+
+template <int KS, int CM>
+__device__ __forceinline__ void load_coeffs(DTile<KS> &dt, int t, const bf16_t *__restrict__ C,
+                                            int64_t ldc, int64_t k, int g) {
+  // C[t, 32 q + 8 g + e].  U's fragments are zero past column k, so a lane
+  // whose columns lie past k may load any finite values: it loads the row's
+  // first columns instead, with no branch and no select, and the values are
+  // first touched by the MFMA.
+  const bf16_t *cr = C + static_cast<int64_t>(t) * ldc;
+#pragma unroll
+  for (int q = 0; q < KS; ++q) {
+    const int64_t c0 = 32 * q + 8 * g;
+    if (CM == 0) {  // 16-byte rows, k % 8 == 0: a chunk is all in or all out
+      dt.b[q] = ld16(cr + (c0 < k ? c0 : 0));
+    } else if (CM == 1) {  // 4-byte rows, k even: pairs are all in or all out
+      const uint32_t *cw = reinterpret_cast<const uint32_t *>(cr);
+      uint32_t w[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int64_t j = c0 + 2 * e2;
+        w[e2] = cw[(j < k ? j : 0) / 2];
+      }
+      dt.b[q] = u32x4{w[0], w[1], w[2], w[3]};
+    } else {
+      uint32_t w[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int64_t j0 = c0 + 2 * e2, j1 = j0 + 1;
+        w[e2] = static_cast<uint32_t>(cr[j0 < k ? j0 : 0]) |
+                (static_cast<uint32_t>(cr[j1 < k ? j1 : 0]) << 16);
+      }
+      dt.b[q] = u32x4{w[0], w[1], w[2], w[3]};
+    }
+  }
+}
+
+// Gathered values in the row layout (rows 4 i + q): T_fixed for both chunks
+// of a tile, P for one chunk.
+struct ERows {
+  u32x4 v[kNC][4];
+};
+struct PRows {
+  u32x4 v[4];
+};
+
+__device__ __forceinline__ void add8(float (&o)[8], u32x4 v) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    o[2 * e] += bf_lo(w[e]);
+    o[2 * e + 1] += bf_hi(w[e]);
+  }
+}
+
+template <int KS, bool HE, bool HP, int CM>
+__global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
+    const bf16_t *__restrict__ rfrag, int64_t k, const bf16_t *__restrict__ C, int64_t ldc,
+    DTiling tm, IdArgs ids, bf16_t *__restrict__ X, int64_t ldx, int ncb, int ntiles,
+    int tiles_per_wg) {
+  constexpr int FR = 2 * KS;  // fragments per row group
+  __shared__ u32x4 us[kPG * FR * 64];
+  __shared__ f32x4 ot[kDW][16 * 32];
+  __shared__ int2 idl[kDW][kMaxWaveTiles][16];  // (token id, position id) per tile row
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // Column block = workgroup index mod the number of blocks: workgroups are
+  // dealt to the 8 XCDs round robin, so each XCD (and its L2) sees only the
+  // columns of ncb / 8 blocks, of U, T_fixed and P alike.
+  const int cb = static_cast<int>(blockIdx.x % static_cast<unsigned>(ncb));
+  const int tg = static_cast<int>(blockIdx.x / static_cast<unsigned>(ncb));
+  const int g = lane >> 4, n = lane & 15;  // MFMA layout
+  const int q = lane >> 4, m = lane & 15;  // row layout
+
+  // each wave takes a contiguous run of the workgroup's tiles
+  const int per_wave = tiles_per_wg / kDW;
+  const int T0 = tg * tiles_per_wg + wave * per_wave;
+  const int T1 = T0 + per_wave < ntiles ? T0 + per_wave : ntiles;
+  const int nt = T0 < T1 ? T1 - T0 : 0;  // this wave's tiles
+
+  // Token of row r of the wave's j-th tile (clamped to the wave's last tile).
+  // Rows past the last token repeat token N-1: they load, compute and store
+  // exactly the bytes of row N-1, so every store is unconditional.
+  auto tile_of = [&](int j) { return static_cast<unsigned>(T0 + (j < nt ? j : nt - 1)); };
+  auto token = [&](unsigned T, int r) {
+    const int t = dtile_token0(tm, T) + r;
+    return t < tm.N ? t : tm.N - 1;
+  };
+
+  // Stage the ids of all the wave's tiles in LDS up front (fixed trip count,
+  // clamped tiles: all loads are in flight before the first wait).
+  if (nt > 0) {
+    int2 v[kMaxWaveTiles / 4];
+#pragma unroll
+    for (int i = 0; i < kMaxWaveTiles / 4; ++i) {
+      const unsigned T = tile_of(4 * i + g);
+      const int t = token(T, n);
+      v[i] = int2{0, 0};
+      if (HE) v[i].x = ids.tok[t];
+      if (HP) {
+        if (ids.pos)
+          v[i].y = ids.pos[t];
+        else if (tm.batch > 0)
+          v[i].y = dtile_pos0(tm, T) + n;
+        else
+          v[i].y = static_cast<int>(static_cast<unsigned>(t) % static_cast<unsigned>(ids.seq_len));
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxWaveTiles / 4; ++i) idl[wave][4 * i + g][n] = v[i];
+  }
+  {  // the block's U slice -> LDS, 1 KiB per direct-to-LDS load
+    const bf16_t *src = rfrag + static_cast<int64_t>(cb) * kPG * FR * 512;
+    for (int f = wave; f < kPG * FR; f += kDW) lds_dma_16(src + f * 512 + lane * 8, us + f * 64);
+    wait_vmcnt<0>();
+  }
+  __syncthreads();
+  if (nt == 0) return;
+
+  const int64_t col_r = static_cast<int64_t>(cb) * kDCols + 8 * m;  // row-layout column
+  f32x4 *otw = ot[wave];
+  int bad = 0;
+
+  auto load_tile = [&](DTile<KS> &dt, int j) {
+    const unsigned T = tile_of(j);
+    load_coeffs<KS, CM>(dt, token(T, n), C, ldc, k, g);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + q;
+      const int t = token(T, r);
+      const int2 v = idl[wave][j < nt ? j : nt - 1][r];
+      if (HE) dt.er[i] = static_cast<int>(clamp_flag(v.x, ids.vocab, 1, bad));
+      if (HP) dt.pr[i] = static_cast<int>(clamp_flag(v.y, ids.n_pos, 2, bad));
+      dt.xr[i] = t;
+    }
+  };
+  const bf16_t *Eb = static_cast<const bf16_t *>(ids.E) + col_r;
+  const bf16_t *Pb = static_cast<const bf16_t *>(ids.P) + col_r;
+  bf16_t *Xb = X + col_r;
+  // The P values are reloaded only when the tile's positions change: in
+  // position-major order a wave's run of tiles holds `batch` tiles with the
+  // same 16 positions in a row, and slot c of the ring keeps chunk c.
+  // T_fixed values are loaded a whole tile ahead (double buffer).  P values
+  // are reloaded only when the tile's positions change: in position-major
+  // order a wave's run of tiles holds `batch` tiles with the same 16
+  // positions in a row; chunk c's P values are refilled right after chunk c
+  // of the previous tile has used them.
+  auto load_e = [&](ERows &er, const DTile<KS> &dt) {
+#pragma unroll
+    for (int c = 0; c < kNC; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        er.v[c][i] = ld16(Eb + static_cast<int64_t>(dt.er[i]) * ids.lde + 128 * c);
+  };
+  auto load_p = [&](PRows &pr, const DTile<KS> &dt, int c) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      pr.v[i] = ld16(Pb + static_cast<int64_t>(dt.pr[i]) * ids.ldp + 128 * c);
+  };
+  // whether tile j has other positions than tile j - 1 (always, unless position-major)
+  auto new_pos = [&](int j) {
+    if (tm.batch == 0 || j == 0) return true;
+    return tile_of(j) / static_cast<unsigned>(tm.batch) !=
+           tile_of(j - 1) / static_cast<unsigned>(tm.batch);
+  };
+
+  // one chunk: MFMAs, transpose through LDS, add the gathered rows, store
+  auto chunk = [&](const DTile<KS> &dt, int c, const ERows &er, const PRows &pr) {
+    f32x4 acc[4][2];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int pg = 4 * c + p;
+      acc[p][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc[p][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int qq = 0; qq < KS; ++qq) {
+        acc[p][0] = mfma(us[((pg * 2 + 0) * KS + qq) * 64 + lane], dt.b[qq], acc[p][0]);
+        acc[p][1] = mfma(us[((pg * 2 + 1) * KS + qq) * 64 + lane], dt.b[qq], acc[p][1]);
+      }
+    }
+    // lane (g, n): token n, columns 32 p + 8 g + 4 h + 0..3 = unit 8 p + 2 g + h
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) otw[ot_slot(n, 8 * p + 2 * g + h)] = acc[p][h];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + q;
+      const f32x4 lo = otw[ot_slot(r, 2 * m)], hi = otw[ot_slot(r, 2 * m + 1)];
+      float o[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      if (HP) add8(o, pr.v[i]);
+      if (HE) add8(o, er.v[c][i]);
+      // Non-temporal store: X is written once and not read back here, and
+      // keeping it out of the caches leaves L2 to the gathered rows (the
+      // gathers' hit rate, and with it the kernel time, depends on it).
+      __builtin_nontemporal_store(
+          u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                pack_bf16x2(o[6], o[7])},
+          reinterpret_cast<u32x4 *>(Xb + static_cast<int64_t>(dt.xr[i]) * ldx + 128 * c));
+    }
+  };
+
+  static_assert(kNC == 2, "two chunks per block");
+  DTile<KS> cur, nxt;
+  ERows eA, eB;
+  PRows p0, p1;
+  load_tile(cur, 0);
+  if (HE) load_e(eA, cur);
+  if (HP) {
+    load_p(p0, cur, 0);
+    load_p(p1, cur, 1);
+  }
+  // tile j: its T_fixed values are in ec, the next tile's go to en
+  auto tile_step = [&](int j, ERows &ec, ERows &en) {
+    // Keep the U fragments in LDS: without this the compiler would hoist
+    // every fragment read out of the loop into registers and halve the
+    // number of resident waves.
+    asm volatile("" ::: "memory");
+    load_tile(nxt, j + 1);  // the last tile repeats itself
+    if (HE) load_e(en, nxt);
+    const bool np1 = HP && j + 1 < nt && new_pos(j + 1);
+    chunk(cur, 0, ec, p0);
+    if (np1) load_p(p0, nxt, 0);
+    chunk(cur, 1, ec, p1);
+    if (np1) load_p(p1, nxt, 1);
+    cur = nxt;
+  };
+  for (int j = 0; j < nt; j += 2) {
+    tile_step(j, eA, eB);
+    if (j + 1 < nt) tile_step(j + 1, eB, eA);
+  }
+  if (bad && ids.err_flag) atomicOr(ids.err_flag, bad);
+}
+
+template <int KS, bool HE, bool HP, int CM>
+void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
+                const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+  const int ncb = static_cast<int>(L.d / kDCols);
+  const int64_t ntiles = ceil_div(tm.N, 16);
+  // about two resident workgroups per CU over the whole grid, whole waves of tiles
+  int64_t per = ceil_div(ntiles * ncb, 512);
+  per = per < kDW ? kDW : (per > kDW * kMaxWaveTiles ? kDW * kMaxWaveTiles : per);
+  per = ceil_div(per, kDW) * kDW;
+  const int64_t tgroups = ceil_div(ntiles, per);
+  dim3 grid(static_cast<unsigned>(tgroups * ncb));
+  decompress_cb_kernel<KS, HE, HP, CM><<<grid, kDThreads, 0, s>>>(
+      rf, L.k, static_cast<const bf16_t *>(C), ldc, tm, ids, static_cast<bf16_t *>(X), ldx, ncb,
+      static_cast<int>(ntiles), static_cast<int>(per));
+}
+
+template <int KS, int CM>
+void launch_dcb_t(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
+                  const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+  const bool he = ids.E != nullptr, hp = ids.P != nullptr;
+  if (he && hp)
+    launch_dcb<KS, true, true, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+  else if (he)
+    launch_dcb<KS, true, false, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+  else if (hp)
+    launch_dcb<KS, false, true, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+  else
+    launch_dcb<KS, false, false, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+}
+
+template <int KS>
+void launch_dcb_ks(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc, int cmode,
+                   const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+  if (cmode == 0)
+    launch_dcb_t<KS, 0>(rf, L, C, ldc, tm, ids, X, ldx, s);
+  else if (cmode == 1)
+    launch_dcb_t<KS, 1>(rf, L, C, ldc, tm, ids, X, ldx, s);
+  else
+    launch_dcb_t<KS, 2>(rf, L, C, ldc, tm, ids, X, ldx, s);
+}
+
+bool table_ok(const void *T, int64_t ld) { return !T || (aligned16(T) && ld % 8 == 0); }
+
+}  // namespace
+
+bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs &ids) {
+  return L.mfma && L.d % kDCols == 0 && aligned16(X) && ldx % 8 == 0 &&
+         table_ok(ids.E, ids.lde) && table_ok(ids.P, ids.ldp);
+}
+
+hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const void *C,
+                                  int64_t N, int64_t ldc, const IdArgs &ids, void *X,
+                                  int64_t ldx, hipStream_t s) {
+  const bf16_t *rf =
+      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_rfrag);
+  // how the coefficient rows may be read: 16-byte chunks, 4-byte pairs, or bf16 by bf16
+  const uintptr_t ca = reinterpret_cast<uintptr_t>(C);
+  const int cmode = (ca & 15) == 0 && ldc % 8 == 0 && L.k % 8 == 0   ? 0
+                    : (ca & 3) == 0 && ldc % 2 == 0 && L.k % 2 == 0 ? 1
+                                                                    : 2;
+  DTiling tm{static_cast<int>(N), 0, 0};
+  // position-major order for the default positions of whole [batch, seq] rows
+  if (ids.P && !ids.pos && ids.seq_len % 16 == 0 && N % ids.seq_len == 0) {
+    tm.seq = static_cast<int>(ids.seq_len);
+    tm.batch = static_cast<int>(N / ids.seq_len);
+  }
+  switch (L.ks) {
+    case 1: launch_dcb_ks<1>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
+    case 2: launch_dcb_ks<2>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
+    case 3: launch_dcb_ks<3>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
+    case 4: launch_dcb_ks<4>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sn
