@@ -30,7 +30,8 @@ constexpr int kBlock = 64 * kWaves;
 
 namespace {
 
-constexpr int kProjCols = 64;  // columns per workgroup in passes 1 and 3
+constexpr int kProjCols = 64;  // columns per workgroup in pass 3
+constexpr int kPadCols = 128;  // m is padded to a multiple of the widest pass-1 slab
 
 struct ProjPlan {
   int64_t m_pad;      // m rounded up to kProjCols
@@ -41,18 +42,31 @@ struct ProjPlan {
   size_t off_tp, off_th, off_tl, total;
 };
 
-ProjPlan proj_plan(int64_t d, int kt, int ks, int64_t m) {
+// Pass 1 splits the rows of W into dsplit ranges when there are too few
+// column slabs to fill the chip; it picks the split that minimises
+// (rounds of workgroups) x (rows per workgroup) for `slots` resident
+// workgroups (slots <= 0: the largest split, for the workspace bound).
+ProjPlan proj_plan(int64_t d, int kt, int ks, int64_t m, int64_t slots) {
   ProjPlan P;
-  P.m_pad = ceil_div(m, kProjCols) * kProjCols;
+  P.m_pad = ceil_div(m, kPadCols) * kPadCols;
   P.kp = 16 * kt;
   P.kp32 = 32 * ks;
-  const int64_t slabs = P.m_pad / kProjCols;
-  int64_t ds = ceil_div(256, slabs);           // aim for >= 256 workgroups
-  const int64_t max_ds = d / 128;               // >= 32 rows per wave
-  if (ds > max_ds) ds = max_ds;
-  if (ds > 8) ds = 8;
-  if (ds < 1) ds = 1;
-  P.rows_per_split = ceil_div(ceil_div(d, ds), 128) * 128;
+  const int64_t slabs = ceil_div(m, 16 * (kt <= 4 ? 8 : 4));  // pass-1 workgroups per split
+  int64_t max_ds = d / 128;  // >= 32 rows per wave
+  if (max_ds > 8) max_ds = 8;
+  if (max_ds < 1) max_ds = 1;
+  int64_t best = max_ds, best_cost = -1;
+  if (slots > 0) {
+    for (int64_t ds = 1; ds <= max_ds; ++ds) {
+      const int64_t rows = ceil_div(ceil_div(d, ds), 128) * 128;
+      const int64_t cost = ceil_div(slabs * ceil_div(d, rows), slots) * rows;
+      if (best_cost < 0 || cost < best_cost) {
+        best = ds;
+        best_cost = cost;
+      }
+    }
+  }
+  P.rows_per_split = ceil_div(ceil_div(d, best), 128) * 128;
   P.dsplit = static_cast<int>(ceil_div(d, P.rows_per_split));
   size_t off = 0;
   P.off_tp = off;
@@ -65,56 +79,101 @@ ProjPlan proj_plan(int64_t d, int kt, int ks, int64_t m) {
   return P;
 }
 
+// Columns per lane in pass 1: 8 (16-byte row loads) while the accumulators
+// fit (KT <= 4), else 4 (8-byte loads).  A wave covers 16 * CW columns.
+template <int KT>
+constexpr int p1_cw() { return KT <= 4 ? 8 : 4; }
+
+template <int CW> struct P1Vec;
+template <> struct P1Vec<8> { typedef u32x4 T; };
+template <> struct P1Vec<4> { typedef u32x2 T; };
+
 template <int KT>
 __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
     const bf16_t *__restrict__ kfrag, int64_t d, const bf16_t *__restrict__ W, int64_t m,
     int64_t ldw, int64_t rows_per_split, int64_t m_pad, float *__restrict__ Tp) {
-  __shared__ f32x4 red[KT][4][64];
+  constexpr int CW = p1_cw<KT>();
+  constexpr int W32 = CW / 2;  // 32-bit words per lane and row
+  typedef typename P1Vec<CW>::T vec;
+  __shared__ f32x4 red[KT][CW][64];
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, n = lane & 15;
-  const int64_t cb = static_cast<int64_t>(blockIdx.x) * kProjCols;
+  const int64_t cb = static_cast<int64_t>(blockIdx.x) * (16 * CW);
   const int split = blockIdx.y;
-  const int64_t col = cb + 4 * n;
-  const bool cvalid = col < m;  // m % 8 == 0: all four columns are valid
+  const int64_t col = cb + CW * n;
+  const bool cvalid = col < m;  // m % 8 == 0: all CW columns are valid
 
   const int steps = static_cast<int>(rows_per_split / 32);
   const int sb = static_cast<int>(split * (rows_per_split / 32));
   const int send = static_cast<int>(d / 32);
-  int s0 = sb + steps * wave / kWaves;
+  const int s0 = sb + steps * wave / kWaves;
   int s1 = sb + steps * (wave + 1) / kWaves;
   if (s1 > send) s1 = send;
 
-  f32x4 acc[KT][4];
+  f32x4 acc[KT][CW];
 #pragma unroll
   for (int t = 0; t < KT; ++t)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[t][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < CW; ++q) acc[t][q] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const bf16_t *wcol = W + col;
+  // Lanes past column m read column 0 instead (any finite values): every
+  // load is unconditional and their columns are never stored.
+  const bf16_t *wcol = W + (cvalid ? col : 0);
   const bf16_t *ufrag = kfrag + lane * 8;
-  for (int s = s0; s < s1; ++s) {
-    u32x2 v[8];
+  // rows 32 s + 8 g + e of the lane's CW columns, and the step's U fragments
+  auto load = [&](int s, vec (&v)[8], u32x4 (&a)[KT]) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int64_t r = 32 * static_cast<int64_t>(s) + 8 * g + e;
-      v[e] = cvalid ? *reinterpret_cast<const u32x2 *>(wcol + r * ldw) : u32x2{0u, 0u};
+    for (int e = 0; e < 8; ++e)
+      v[e] = *reinterpret_cast<const vec *>(wcol + (32 * static_cast<int64_t>(s) + 8 * g + e) * ldw);
+#pragma unroll
+    for (int t = 0; t < KT; ++t) a[t] = ld16(ufrag + (static_cast<int64_t>(s) * KT + t) * 512);
+  };
+  auto word = [](const vec &v, int w) -> uint32_t {
+    if constexpr (CW == 8) return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+    else return w == 0 ? v.x : v.y;
+  };
+  auto step = [&](const vec (&v)[8], const u32x4 (&a)[KT]) {
+    // 8 x CW block (rows e, columns q) -> CW B operands of 8 rows each
+#pragma unroll
+    for (int w = 0; w < W32; ++w) {
+      u32x4 b0, b1;  // columns 2 w and 2 w + 1
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo = word(v[2 * i], w), hi = word(v[2 * i + 1], w);
+        b0[i] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // low halves
+        b1[i] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);  // high halves
+      }
+#pragma unroll
+      for (int t = 0; t < KT; ++t) {
+        acc[t][2 * w] = mfma(a[t], b0, acc[t][2 * w]);
+        acc[t][2 * w + 1] = mfma(a[t], b1, acc[t][2 * w + 1]);
+      }
     }
-    u32x4 b[4];
+  };
+
+  // PD-deep ring of row steps in flight (memory latency under load is long
+  // and there is one wave per SIMD): step s + PD is loaded as soon as step s
+  // has been consumed; past the end the last step is reloaded.
+  constexpr int PD = 4;
+  if (s0 < s1) {
+    vec v[PD][8];
+    u32x4 a[PD][KT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const u32x2 lo = v[2 * i], hi = v[2 * i + 1];
-      b[0][i] = (lo.x & 0xFFFFu) | (hi.x << 16);
-      b[1][i] = (lo.x >> 16) | (hi.x & 0xFFFF0000u);
-      b[2][i] = (lo.y & 0xFFFFu) | (hi.y << 16);
-      b[3][i] = (lo.y >> 16) | (hi.y & 0xFFFF0000u);
+    for (int r = 0; r < PD; ++r) load(s0 + r < s1 ? s0 + r : s1 - 1, v[r], a[r]);
+    int s = s0;
+    for (; s + PD <= s1; s += PD) {  // whole groups: no guards in the loop body
+#pragma unroll
+      for (int r = 0; r < PD; ++r) {
+        step(v[r], a[r]);
+        const int sn = s + r + PD;
+        load(sn < s1 ? sn : s1 - 1, v[r], a[r]);
+        __builtin_amdgcn_sched_barrier(0);  // keep the refill here
+      }
     }
 #pragma unroll
-    for (int t = 0; t < KT; ++t) {
-      const u32x4 a = ld16(ufrag + (static_cast<int64_t>(s) * KT + t) * 512);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc[t][q] = mfma(a, b[q], acc[t][q]);
-    }
+    for (int r = 0; r < PD; ++r)
+      if (s + r < s1) step(v[r], a[r]);
   }
 
   // fixed-order reduction: acc0 + (acc1 + (acc2 + acc3))
@@ -123,7 +182,7 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
 #pragma unroll
       for (int t = 0; t < KT; ++t)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < CW; ++q) {
           f32x4 v = acc[t][q];
           if (w < kWaves - 1) v += red[t][q][lane];
           red[t][q][lane] = v;
@@ -136,7 +195,7 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
 #pragma unroll
     for (int t = 0; t < KT; ++t)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < CW; ++q) {
         const f32x4 v = acc[t][q] + red[t][q][lane];
         float *dst = Tp + ((static_cast<int64_t>(split) * m_pad + col + q) * (16 * KT)) + 16 * t + 4 * g;
         *reinterpret_cast<f32x4 *>(dst) = v;
@@ -172,7 +231,7 @@ __global__ __launch_bounds__(kBlock) void project_pass3_kernel(
     const bf16_t *__restrict__ Tl, bf16_t *__restrict__ W, int64_t m, int64_t ldw,
     int64_t rows_per_block) {
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, n = lane & 15;
   const int64_t cb = static_cast<int64_t>(blockIdx.x) * kProjCols;
 
@@ -197,13 +256,16 @@ __global__ __launch_bounds__(kBlock) void project_pass3_kernel(
   if (p1 > pend) p1 = pend;
   const bf16_t *ufrag = rfrag + lane * 8;
 
-  for (int p = p0; p < p1; ++p) {
-    u32x4 b[2][KS];
+  // U fragments of row group p (loaded one group ahead; past the end the
+  // last group is reloaded)
+  auto load_u = [&](int p, u32x4 (&b)[2][KS]) {
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int q = 0; q < KS; ++q)
         b[h][q] = ld16(ufrag + ((static_cast<int64_t>(p) * 2 + h) * KS + q) * 512);
+  };
+  auto group = [&](int p, const u32x4 (&b)[2][KS]) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int64_t r = 32 * static_cast<int64_t>(p) + 8 * (n >> 2) + 4 * h + (n & 3);
@@ -230,13 +292,25 @@ __global__ __launch_bounds__(kBlock) void project_pass3_kernel(
         }
       }
     }
+  };
+  if (p0 < p1) {
+    u32x4 b0[2][KS], b1[2][KS];
+    load_u(p0, b0);
+    int p = p0;
+    for (; p + 2 <= p1; p += 2) {
+      load_u(p + 1, b1);
+      group(p, b0);
+      load_u(p + 2 < p1 ? p + 2 : p1 - 1, b0);
+      group(p + 1, b1);
+    }
+    if (p < p1) group(p, b0);
   }
 }
 
 template <int KT>
 void launch_p1(const ProjPlan &P, const bf16_t *kf, int64_t d, const bf16_t *W, int64_t m,
                int64_t ldw, float *Tp, hipStream_t s) {
-  dim3 grid(static_cast<unsigned>(P.m_pad / kProjCols), static_cast<unsigned>(P.dsplit));
+  dim3 grid(static_cast<unsigned>(ceil_div(m, 16 * p1_cw<KT>())), static_cast<unsigned>(P.dsplit));
   project_pass1_kernel<KT><<<grid, kBlock, 0, s>>>(kf, d, W, m, ldw, P.rows_per_split, P.m_pad,
                                                    Tp);
 }
@@ -255,11 +329,37 @@ void launch_p3(const ProjPlan &P, const bf16_t *rf, int64_t d, const bf16_t *Th,
   project_pass3_kernel<KS><<<grid, kBlock, 0, s>>>(rf, d, Th, Tl, W, m, ldw, rows);
 }
 
+template <int KT>
+int64_t slots_kt() {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, reinterpret_cast<const void *>(project_pass1_kernel<KT>), kBlock, 0) !=
+          hipSuccess)
+    return 256;
+  return static_cast<int64_t>(cus) * (per_cu > 0 ? per_cu : 1);
+}
+
+// resident pass-1 workgroups on the current device
+int64_t pass1_slots(int kt) {
+  switch (kt) {
+    case 1: return slots_kt<1>();
+    case 2: return slots_kt<2>();
+    case 3: return slots_kt<3>();
+    case 4: return slots_kt<4>();
+    case 5: return slots_kt<5>();
+    case 6: return slots_kt<6>();
+    case 7: return slots_kt<7>();
+    default: return slots_kt<8>();
+  }
+}
+
 }  // namespace
 
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m) {
   const int kt = static_cast<int>(ceil_div(k, 16)), ks = static_cast<int>(ceil_div(k, 32));
-  return proj_plan(d, kt, ks, m).total;
+  return proj_plan(d, kt, ks, m, 0).total;  // the largest split bounds every plan
 }
 
 bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw) {
@@ -268,7 +368,7 @@ bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw)
 
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s) {
-  const ProjPlan P = proj_plan(L.d, L.kt, L.ks, m);
+  const ProjPlan P = proj_plan(L.d, L.kt, L.ks, m, pass1_slots(L.kt));
   const char *base = static_cast<const char *>(packed);
   const bf16_t *kf = reinterpret_cast<const bf16_t *>(base + L.off_kfrag);
   const bf16_t *rf = reinterpret_cast<const bf16_t *>(base + L.off_rfrag);
