@@ -3,7 +3,7 @@
 One step = the whole hot path for one batch at d=4096, k=40, N=32768 tokens
 (8 x 4096), bf16, vocab 32000 with Zipf(1.1) ids:
 
-  compress      C  = (X - P[pos] - E[tok]) U
+  compress      C  = (X - P[pos] - E[tok]) U      gather + subtract + projection, one kernel
   decompress    X' = C U^T + P[pos] + E[tok]
   grad compress Cg = G U
   grad decomp.  G' = Cg U^T
@@ -15,11 +15,21 @@ Infinity Cache.  Prints one JSON line.  ``value`` is the step's algorithmic
 bytes (each op's inputs and outputs, each unique gathered embedding row once,
 U once per op) over the step time.
 
+Also reported, outside the step: the same compress computed against
+projected tables (sn_embed_project once per basis, then
+sn_compress_projected), the path to use while U is fixed between subspace
+updates.
+
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py --profile-pass                    # short run for rocprofv3 counters
+    python bench.py --traffic-summary FETCH_DIR WRITE_DIR   # writes profiles/traffic_*.json/.md
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -31,6 +41,18 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+CFG_ID = 2
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_codec_step_d4096_k40.json")
+CALIB_BYTES = 256 * 1024 * 1024   # plain copy used to scale the HBM counters
+
+# rocprofv3 kernel names of each op (substring match on the demangled name)
+OP_KERNELS = {
+    "compress": ["compress_kernel<3, true, true, true>"],
+    "decompress": ["decompress_cb_kernel<2, true, true, 0>"],
+    "grad_compress": ["stream_compress_kernel<3, 0>"],
+    "grad_decompress": ["decompress_cb_kernel<2, false, false, 0>"],
+    "compress_projected": ["stream_compress_kernel<3, 1>"],
+}
 
 
 def parse():
@@ -42,7 +64,21 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=32768,
                     help="tokens in the oracle's timed sample")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="run a few steps and a plain copy of known size, print nothing")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE)")
     return ap.parse_args()
+
+
+def source_hash() -> str:
+    """Hash of the HIP / C++ sources: a traffic figure is valid for one build only."""
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2506_01260_amd", "csrc", "*"))):
+        h.update(os.path.basename(p).encode())
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def to_dev(a, bf16=True):
@@ -86,8 +122,103 @@ def cpu_baseline(w, weights, rows: int):
             "seconds": dt}
 
 
+# --------------------------------------------------------------------------- counters
+
+def _counter_rows(d: str):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    for f in files:
+        yield from csv.DictReader(open(f))
+
+
+def _per_kernel(d: str, counter: str):
+    """Mean counter value (KiB per dispatch) per kernel name."""
+    acc: dict = {}
+    for r in _counter_rows(d):
+        if r["Counter_Name"] != counter:
+            continue
+        acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return {k: float(np.mean(v)) for k, v in acc.items()}
+
+
+def _short(name: str) -> str:
+    """Kernel name without its argument list and namespaces."""
+    base = name.split(">(")[0] + ">" if ">(" in name else name.split("(unsigned")[0]
+    return base.replace("void ", "").replace("sn::", "").replace("(anonymous namespace)::", "")
+
+
+def traffic_summary(fetch_dir: str, write_dir: str):
+    fetch = _per_kernel(fetch_dir, "FETCH_SIZE")
+    write = _per_kernel(write_dir, "WRITE_SIZE")
+
+    def find(table, subs, also=None):
+        for name, v in table.items():
+            if any(s in name for s in subs) and (also is None or also in name):
+                return name, v
+        return None, None
+
+    # the calibration kernel is the only multiply of the pass
+    cname, cf = find(fetch, ["MulFunctor"])
+    _, cw = find(write, ["MulFunctor"])
+    if cf is None or cw is None:
+        raise SystemExit("calibration copy kernel not found in the counter files")
+    f_scale = CALIB_BYTES / (cf * 1024.0)
+    w_scale = CALIB_BYTES / (cw * 1024.0)
+    out = {"source_hash": source_hash(),
+           "calibration": {"kernel": cname, "bytes_read": CALIB_BYTES, "bytes_written": CALIB_BYTES,
+                           "fetch_kib": cf, "write_kib": cw,
+                           "fetch_scale": f_scale, "write_scale": w_scale},
+           "ops": {}}
+    for op, subs in OP_KERNELS.items():
+        name, fv = find(fetch, subs)
+        _, wv = find(write, subs)
+        if fv is None or wv is None:
+            continue
+        fb, wb = fv * 1024.0 * f_scale, wv * 1024.0 * w_scale
+        out["ops"][op] = {"kernel": _short(name), "fetch_kib": fv, "write_kib": wv,
+                          "fetch_bytes": fb, "write_bytes": wb, "traffic_bytes": fb + wb}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    md = TRAFFIC_FILE[:-5] + ".md"
+    with open(md, "w") as f:
+        f.write("# HBM traffic per launch: codec step at d=4096, k=40, N=32768 (bf16)\n\n")
+        f.write("Commands (repository root on the GPU box as `$R`; `cd /tmp && export "
+                "TMPDIR=/tmp` first), one counter per run:\n\n```\n"
+                "rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/pmc_fetch -o f --output-format csv "
+                "-- python3 $R/bench.py --profile-pass\n"
+                "rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/pmc_write -o w --output-format csv "
+                "-- python3 $R/bench.py --profile-pass\n"
+                "python3 bench.py --traffic-summary gpurun_out/pmc_fetch gpurun_out/pmc_write\n```\n\n")
+        f.write(f"Scale: a streaming kernel (`y = 1.0 * x`, fp32) that reads and writes "
+                f"{CALIB_BYTES} bytes (torch `mul` fp32 elementwise kernel) "
+                f"reads {cf:.0f} KiB and writes {cw:.0f} KiB per dispatch; counters are "
+                f"multiplied by {f_scale:.4f} (fetch) and {w_scale:.4f} (write).\n\n")
+        f.write(f"Source hash `{out['source_hash']}`.\n\n")
+        f.write("| op | kernel | fetch MB | write MB | traffic MB |\n|---|---|---|---|---|\n")
+        for op, v in out["ops"].items():
+            f.write(f"| {op} | `{v['kernel']}` | "
+                    f"{v['fetch_bytes'] / 1e6:.1f} | {v['write_bytes'] / 1e6:.1f} | "
+                    f"{v['traffic_bytes'] / 1e6:.1f} |\n")
+    print(json.dumps(out, indent=1))
+
+
+def load_traffic():
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    return t if t.get("source_hash") == source_hash() else None
+
+
+# --------------------------------------------------------------------------- main
+
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
               f"multi-GPU path", file=sys.stderr)
@@ -97,8 +228,7 @@ def main():
     import synth
     import paper_2506_01260_amd as sn
 
-    cfg_id = 2
-    w = synth.make_workload(cfg_id)
+    w = synth.make_workload(CFG_ID)
     cfg = w["cfg"]
     N, d, k = cfg.n_tokens, cfg.d, cfg.k
     print(f"[bench] inputs generated: N={N} d={d} k={k}", file=sys.stderr, flush=True)
@@ -112,11 +242,12 @@ def main():
     Gs = [to_dev(w["G"]) for _ in range(R)]
     Cs = [torch.empty(N, k, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     Cgs = [torch.empty(N, k, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    Cps = [torch.empty(N, k, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     Xrs = [torch.empty(N, d, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     Grs = [torch.empty(N, d, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     weights, host_weights = [], []
     for i, (rows, cols) in enumerate(cfg.weights):
-        wb = synth.make_weight(cfg_id, i, rows, cols)
+        wb = synth.make_weight(CFG_ID, i, rows, cols)
         host_weights.append(wb)
         base = to_dev(wb)
         weights.append([base.clone() for _ in range(R)])
@@ -125,11 +256,13 @@ def main():
                    for _, c in cfg.weights)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
 
-    # algorithmic bytes per op
+    # algorithmic bytes per op: inputs and outputs, each unique gathered row once, U once
     es = 2
-    uniq_e = len(np.unique(w["tok"])) * d * es
+    uniq_tok = len(np.unique(w["tok"]))
+    uniq_e = uniq_tok * d * es
     uniq_p = min(cfg.seq, N) * d * es
     xb, cb, ub = N * d * es, N * k * es, d * k * es
+    kp = 16 * ((k + 15) // 16)
     op_bytes = {
         "compress": xb + cb + uniq_e + uniq_p + ub,
         "decompress": cb + xb + uniq_e + uniq_p + ub,
@@ -138,6 +271,12 @@ def main():
     }
     for i, (rows, cols) in enumerate(cfg.weights):
         op_bytes[f"project_W{i}"] = 2 * rows * cols * es
+    # the projected-table compress reads k-wide fp32 projected rows instead of d-wide ones
+    alt_bytes = {"compress_projected": xb + cb + ub + (uniq_tok + min(cfg.seq, N)) * kp * 4,
+                 "embed_project": (cfg.vocab + cfg.seq) * d * es + (cfg.vocab + cfg.seq) * kp * 4
+                 + ub}
+
+    proj = sn.sn_embed_project(basis, E=E, P=P)
 
     def op(name, i):
         j = i % R
@@ -149,6 +288,10 @@ def main():
             sn.sn_grad_compress(basis, Gs[j], out=Cgs[j])
         elif name == "grad_decompress":
             sn.sn_decompress(basis, Cgs[j], out=Grs[j])
+        elif name == "compress_projected":
+            sn.sn_compress_projected(basis, Xs[j], proj, tok=tok, seq_len=cfg.seq, out=Cps[j])
+        elif name == "embed_project":
+            sn.sn_embed_project(basis, E=E, P=P)
         else:
             wi = int(name[len("project_W"):])
             sn.sn_project_weights(basis, weights[wi][j], workspace=ws)
@@ -164,15 +307,28 @@ def main():
             if evs is not None:
                 evs[nm][1].record(stream)
 
+    if args.profile_pass:
+        # plain streaming kernel of known traffic: reads and writes CALIB_BYTES
+        src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        for i in range(3):
+            step(i)
+            op("compress_projected", i)
+        torch.cuda.synchronize()
+        print("[bench] profile pass done", file=sys.stderr, flush=True)
+        return
+
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
     K = args.steps
-    evs = [{nm: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for nm in names} for _ in range(K)]
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))  # noqa: E731
+    evs = [{nm: mk() for nm in names} for _ in range(K)]
+    t_start, t_end = mk()
     torch.cuda.synchronize()
     t_start.record(stream)
     for i in range(K):
@@ -181,20 +337,44 @@ def main():
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / K
-    op_ms = {nm: float(np.mean([e[nm][0].elapsed_time(e[nm][1]) for e in evs])) for nm in names}
+    samples = {nm: np.array([e[nm][0].elapsed_time(e[nm][1]) for e in evs]) for nm in names}
+    op_ms = {nm: float(np.mean(v)) for nm, v in samples.items()}
     print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # the projected-table compress, back to back over the same buffer rotation
+    # (the tables are rebuilt once, as after a subspace update)
+    alt_samples = {"compress_projected": [], "embed_project": []}
+    for i in range(K + 1):
+        nm = "embed_project" if i == 0 else "compress_projected"
+        a, b = mk()
+        a.record(stream)
+        op(nm, args.warmup + i)
+        b.record(stream)
+        alt_samples[nm].append((a, b))
+    torch.cuda.synchronize()
+    alt_ms = {nm: float(np.mean([a.elapsed_time(b) for a, b in v])) for nm, v in alt_samples.items()}
 
     step_bytes = sum(op_bytes.values())
     value = step_bytes / (ms_step * 1e-3) / 1e9
-    ops = {nm: {"ms": round(op_ms[nm], 5), "bytes": op_bytes[nm],
-                "GBps": round(op_bytes[nm] / (op_ms[nm] * 1e-3) / 1e9, 1),
-                "frac_hbm": round(op_bytes[nm] / (op_ms[nm] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    def rate(nbytes, ms):
+        return nbytes / (ms * 1e-3) / 1e9
+
+    ops = {nm: {"ms": round(op_ms[nm], 5), "ms_median": round(float(np.median(samples[nm])), 5),
+                "ms_min": round(float(np.min(samples[nm])), 5), "bytes": op_bytes[nm],
+                "GBps": round(rate(op_bytes[nm], op_ms[nm]), 1),
+                "frac_hbm": round(rate(op_bytes[nm], op_ms[nm]) / HBM_PEAK_GBS, 4)}
            for nm in names}
     pair_ms = op_ms["compress"] + op_ms["decompress"]
     pair_bytes = op_bytes["compress"] + op_bytes["decompress"]
-    pair_gbs = pair_bytes / (pair_ms * 1e-3) / 1e9
+    ppair_ms = alt_ms["compress_projected"] + op_ms["decompress"]
+    ppair_bytes = alt_bytes["compress_projected"] + op_bytes["decompress"]
     dom = max(names, key=lambda nm: op_ms[nm])
-    dom_gbs = op_bytes[dom] / (op_ms[dom] * 1e-3) / 1e9
+    dom_gbs = rate(op_bytes[dom], op_ms[dom])
+    traffic = load_traffic()
+    dom_traffic = None
+    if traffic and dom in traffic.get("ops", {}):
+        dom_traffic = round(traffic["ops"][dom]["traffic_bytes"])
 
     out = {
         "metric": "codec GB/s & % HBM peak (compress+decompress) at d=4096,k=40; tokens/s",
@@ -214,16 +394,26 @@ def main():
                                "Zipf(1.1) + in-place projection of Wo 4096x4096 and "
                                "W2 4096x14336, bf16",
                    "d": d, "k": k, "tokens": N, "seq_len": cfg.seq, "vocab": cfg.vocab,
-                   "rotate_buffers": R},
+                   "unique_tokens": uniq_tok, "rotate_buffers": R},
         "tokens_per_s": round(N / (ms_step * 1e-3), 1),
         "codec_pair": {"ops": "compress+decompress", "ms": round(pair_ms, 5),
-                       "GBps": round(pair_gbs, 1), "frac_hbm": round(pair_gbs / HBM_PEAK_GBS, 4),
+                       "GBps": round(rate(pair_bytes, pair_ms), 1),
+                       "frac_hbm": round(rate(pair_bytes, pair_ms) / HBM_PEAK_GBS, 4),
                        "tokens_per_s": round(N / (pair_ms * 1e-3), 1),
-                       "x_c_only_GBps": round(2 * (xb + cb) / (pair_ms * 1e-3) / 1e9, 1)},
+                       "x_c_only_GBps": round(rate(2 * (xb + cb), pair_ms), 1)},
+        "codec_pair_projected": {
+            "ops": "compress_projected+decompress (tables built once per basis)",
+            "ms": round(ppair_ms, 5), "GBps": round(rate(ppair_bytes, ppair_ms), 1),
+            "frac_hbm": round(rate(ppair_bytes, ppair_ms) / HBM_PEAK_GBS, 4),
+            "tokens_per_s": round(N / (ppair_ms * 1e-3), 1),
+            "compress_projected_ms": round(alt_ms["compress_projected"], 5),
+            "embed_project_ms": round(alt_ms["embed_project"], 5),
+            "embed_project_per_step_at_500_steps_ms": round(alt_ms["embed_project"] / 500, 6)},
         "ops": ops,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(dom_gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": dom_traffic,
+                     "algorithmic_bytes": op_bytes[dom]},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)

@@ -1,28 +1,26 @@
-// The bf16 stage-boundary codec on the gfx950 matrix cores.
+// The bf16 compress kernels on the gfx950 matrix cores (decompress is in
+// sn_decompress.hip, the weight projection in sn_project.hip).
 //
 // compress   C[i, :] = (X[i, :] - P[pos_i, :] - E[tok_i, :]) U      (Sec. 4.3.1, Eq. "subtract")
 //            D[j, token] = sum_r U[r, j] * (X - P - E)[token, r], computed as
 //            X U + (-P) U + (-E) U in one set of fp32 accumulators (sign-flipped
 //            bf16 operands), so X - P - E is never rounded: every bf16 product
 //            is exact and every sum is fp32.
-// decompress X[i, :] = C[i, :] U^T + P[pos_i, :] + E[tok_i, :]       (Sec. 4.3.1, recovery)
-//            D[r, token] = sum_j U[r, j] C[token, j], then + P + E in fp32.
-// Without tables these are the gradient codec of Sec. 4.4.
+// Without tables this is the gradient compress of Sec. 4.4.
 //
-// Structure (one workgroup = 4 compute waves + 1 producer wave, 64 tokens):
+// compress_kernel (one workgroup = 4 compute waves + 1 producer wave, 64 tokens):
 //
 // * The producer wave copies, for each stage of 128 columns of d, everything
 //   the compute waves need into one of NB LDS buffers with direct-to-LDS
-//   loads: the 64 tokens' X rows (compress), their E and P rows, and the U
-//   fragments of the stage.  Each copy instruction reads 4 rows x 256
-//   contiguous bytes (contiguous row pieces are much cheaper for the memory
-//   pipeline than the 16-rows-x-64-bytes pattern of an MFMA operand), and the
-//   16-byte pieces of row r are stored in the order p ^ (r & 7) so that the
-//   compute waves' operand reads (16 rows, same piece) hit distinct banks.
+//   loads: the 64 tokens' X rows, their E and P rows, and the U fragments of
+//   the stage.  Each copy instruction reads 4 rows x 256 contiguous bytes
+//   (contiguous row pieces are much cheaper for the memory pipeline than the
+//   16-rows-x-64-bytes pattern of an MFMA operand), and the 16-byte pieces of
+//   row r are stored in the order p ^ (r & 7) so that the compute waves'
+//   operand reads (16 rows, same piece) hit distinct banks.
 // * Compute wave w owns 16 tokens and the whole of d; it reads operands only
 //   from LDS (no global loads in its main loop), so nothing stalls it but the
-//   hand-over barrier.  Decompress stages each output tile in LDS and writes
-//   it back with 256-byte row pieces.
+//   hand-over barrier.
 // * NB-deep buffering: the producer keeps NB-1 stages in flight; one barrier
 //   per stage hands a buffer over.  Workgroups start at different stages
 //   (rotation) so the rows in flight across the chip are not read at the same
@@ -30,6 +28,9 @@
 // * Position-major tiles (positions i mod seq_len, batch a multiple of 4): a
 //   16-token tile holds 16/B consecutive positions of B batches, so the tile
 //   needs only 16/B positional rows.
+//
+// stream_compress_kernel (X U with no gathered rows) is described at its
+// definition.
 #include "sn_mfma_common.h"
 
 namespace sn {
@@ -77,7 +78,7 @@ template <bool PM>
 constexpr int p_rows() { return PM ? 16 : kTokens; }  // positional rows staged per workgroup
 
 // ---------------------------------------------------------------------------
-// Stage buffer geometry (in 16-byte units) for compress / decompress.
+// Stage buffer geometry (in 16-byte units) of compress_kernel.
 // ---------------------------------------------------------------------------
 template <int KT, bool HE, bool HP, bool PM>
 struct CGeo {
