@@ -23,6 +23,7 @@ updates.
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
     python bench.py --profile-pass                    # short run for rocprofv3 counters
     python bench.py --traffic-summary FETCH_DIR WRITE_DIR   # writes profiles/traffic_*.json/.md
+    python bench.py --trace-summary TRACE_DIR BENCH_LOG     # writes profiles/*_kernel_stats.md
 """
 from __future__ import annotations
 
@@ -68,6 +69,9 @@ def parse():
                     help="run a few steps and a plain copy of known size, print nothing")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE)")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_LOG"),
+                    help="summarise a rocprofv3 --kernel-trace run of this script, split by "
+                         "phase, beside the JSON line that run printed")
     return ap.parse_args()
 
 
@@ -144,8 +148,8 @@ def _per_kernel(d: str, counter: str):
 
 def _short(name: str) -> str:
     """Kernel name without its argument list and namespaces."""
-    base = name.split(">(")[0] + ">" if ">(" in name else name.split("(unsigned")[0]
-    return base.replace("void ", "").replace("sn::", "").replace("(anonymous namespace)::", "")
+    name = name.replace("void ", "").replace("sn::", "").replace("(anonymous namespace)::", "")
+    return name.split(">(")[0] + ">" if ">(" in name else name.split("(")[0]
 
 
 def traffic_summary(fetch_dir: str, write_dir: str):
@@ -204,6 +208,81 @@ def traffic_summary(fetch_dir: str, write_dir: str):
     print(json.dumps(out, indent=1))
 
 
+def trace_summary(trace_dir: str, bench_log: str):
+    """Per-kernel durations of a ``rocprofv3 --kernel-trace`` run of this
+    script, split into the phases main() runs in order: set-up, the warm-up
+    and timed steps, the two back-to-back pair loops, the table build and the
+    projected compress alone.  Only this library's kernels are counted; the
+    phases are found from the dispatch order (a step starts at each compress
+    launch and has a fixed number of launches)."""
+    files = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_trace.csv under {trace_dir}")
+    rows = [r for f in files for r in csv.DictReader(open(f)) if "sn::" in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    line = next((ln for ln in open(bench_log) if ln.startswith("{\"metric\"")), None)
+    if line is None:
+        raise SystemExit(f"no JSON line in {bench_log}")
+    b = json.loads(line)
+    W, K = b["warmup"], b["steps"]
+    names = [_short(r["Kernel_Name"]) for r in rows]
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    comp = _short(next(r["Kernel_Name"] for r in rows if OP_KERNELS["compress"][0] in r["Kernel_Name"]))
+    starts = [i for i, n in enumerate(names) if n == comp]
+    s0, per_step = starts[0], starts[1] - starts[0]
+    pair = 2 * (3 + K)
+    cuts = [("set-up", 0, s0),
+            ("warm-up steps", s0, s0 + W * per_step),
+            ("timed steps", s0 + W * per_step, s0 + (W + K) * per_step),
+            ("timed steps, event per op", s0 + (W + K) * per_step, s0 + (W + 2 * K) * per_step)]
+    e = cuts[-1][2]
+    cuts += [("compress+decompress loop, warm-up", e, e + 6),
+             ("compress+decompress loop, timed", e + 6, e + pair),
+             ("compress_projected+decompress loop, warm-up", e + pair, e + pair + 6),
+             ("compress_projected+decompress loop, timed", e + pair + 6, e + 2 * pair),
+             ("table build", e + 2 * pair, len(rows) - K),
+             ("compress_projected alone", len(rows) - K, len(rows))]
+    if cuts[-1][1] < cuts[-2][1]:
+        raise SystemExit("dispatch count does not match the bench's phase layout")
+    out = os.path.join(ROOT, "profiles", "codec_step_d4096_k40_kernel_stats.md")
+    with open(out, "w") as f:
+        f.write("# Kernel durations: codec step at d=4096, k=40, N=32768 (bf16)\n\n")
+        f.write("Commands (repository root on the GPU box as `$R`; `cd /tmp && export "
+                "TMPDIR=/tmp` first):\n\n```\n"
+                f"rocprofv3 --kernel-trace --stats -d $R/gpurun_out/prof_step -o step "
+                f"--output-format csv -- python3 $R/bench.py --steps {K} --warmup {W} "
+                f"--no-cpu-baseline > $R/gpurun_out/prof_step.log\n"
+                "python3 bench.py --trace-summary gpurun_out/prof_step gpurun_out/prof_step.log\n"
+                "```\n\n")
+        f.write(f"Source hash `{source_hash()}`. Durations are rocprofv3's kernel begin/end "
+                f"timestamps; the bench's own figures (HIP events around each launch on the "
+                f"launch stream, same run) are in the last column where the phase is the one "
+                f"they time.\n\n")
+        f.write("| phase | kernel | calls | average (us) | min (us) | max (us) | bench event "
+                "mean (us) |\n|---|---|---|---|---|---|---|\n")
+        for phase, lo, hi in cuts:
+            seen = []
+            for n in names[lo:hi]:
+                if n not in seen:
+                    seen.append(n)
+            for n in seen:
+                ds = [dur[i] for i in range(lo, hi) if names[i] == n]
+                ev = ""
+                if phase == "timed steps, event per op":
+                    ops_here = [op for op, subs in OP_KERNELS.items() if n in subs]
+                    if ops_here and ops_here[0] in b["ops"]:
+                        ev = f"{b['ops'][ops_here[0]]['ms'] * 1e3:.1f}"
+                elif phase == "compress_projected alone":
+                    ev = f"{b['codec_pair_projected']['compress_projected_ms'] * 1e3:.1f}"
+                f.write(f"| {phase} | `{n}` | {len(ds)} | {np.mean(ds):.1f} | {np.min(ds):.1f} "
+                        f"| {np.max(ds):.1f} | {ev} |\n")
+        f.write("\nBench line of the same run (HIP events):\n\n```\n")
+        f.write(json.dumps({"value": b["value"], "unit": b["unit"],
+                            "ms_per_step": b["ms_per_step"], "roofline": b["roofline"],
+                            "codec_pair": b["codec_pair"]}) + "\n```\n")
+    print(open(out).read())
+
+
 def load_traffic():
     try:
         t = json.load(open(TRAFFIC_FILE))
@@ -218,6 +297,9 @@ def main():
     args = parse()
     if args.traffic_summary:
         traffic_summary(*args.traffic_summary)
+        return
+    if args.trace_summary:
+        trace_summary(*args.trace_summary)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
@@ -327,19 +409,49 @@ def main():
 
     K = args.steps
     mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))  # noqa: E731
-    evs = [{nm: mk() for nm in names} for _ in range(K)]
+    # the step time: K steps with events only at the two ends
     t_start, t_end = mk()
     torch.cuda.synchronize()
     t_start.record(stream)
     for i in range(K):
-        step(args.warmup + i, evs[i])
+        step(args.warmup + i)
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / K
+    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+    # per-op times: K more steps with an event pair around every launch (the
+    # marker packets add a few microseconds per op, so these sum to more than
+    # the step time above)
+    evs = [{nm: mk() for nm in names} for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        step(args.warmup + K + i, evs[i])
+    torch.cuda.synchronize()
     samples = {nm: np.array([e[nm][0].elapsed_time(e[nm][1]) for e in evs]) for nm in names}
     op_ms = {nm: float(np.mean(v)) for nm, v in samples.items()}
-    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+    print(f"[bench] timed {K} steps per op", file=sys.stderr, flush=True)
+
+    # Steady-state codec pair: compress then decompress, back to back over the
+    # buffer rotation.  Timing the pair as a whole charges each iteration for
+    # the write-backs the previous one left in the caches, which the per-op
+    # event times inside the step can shift from one op to the next.
+    def pair_loop(cname):
+        a, b = mk()
+        for i in range(3):
+            op(cname, i)
+            op("decompress", i)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(K):
+            op(cname, args.warmup + i)
+            op("decompress", args.warmup + i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    pair_ms = pair_loop("compress")
+    ppair_ms = pair_loop("compress_projected")
 
     # the projected-table compress, back to back over the same buffer rotation
     # (the tables are rebuilt once, as after a subspace update)
@@ -365,9 +477,7 @@ def main():
                 "GBps": round(rate(op_bytes[nm], op_ms[nm]), 1),
                 "frac_hbm": round(rate(op_bytes[nm], op_ms[nm]) / HBM_PEAK_GBS, 4)}
            for nm in names}
-    pair_ms = op_ms["compress"] + op_ms["decompress"]
     pair_bytes = op_bytes["compress"] + op_bytes["decompress"]
-    ppair_ms = alt_ms["compress_projected"] + op_ms["decompress"]
     ppair_bytes = alt_bytes["compress_projected"] + op_bytes["decompress"]
     dom = max(names, key=lambda nm: op_ms[nm])
     dom_gbs = rate(op_bytes[dom], op_ms[dom])
@@ -396,13 +506,14 @@ def main():
                    "d": d, "k": k, "tokens": N, "seq_len": cfg.seq, "vocab": cfg.vocab,
                    "unique_tokens": uniq_tok, "rotate_buffers": R},
         "tokens_per_s": round(N / (ms_step * 1e-3), 1),
-        "codec_pair": {"ops": "compress+decompress", "ms": round(pair_ms, 5),
+        "codec_pair": {"ops": "compress+decompress, back to back", "ms": round(pair_ms, 5),
+                       "in_step_ms": round(op_ms["compress"] + op_ms["decompress"], 5),
                        "GBps": round(rate(pair_bytes, pair_ms), 1),
                        "frac_hbm": round(rate(pair_bytes, pair_ms) / HBM_PEAK_GBS, 4),
                        "tokens_per_s": round(N / (pair_ms * 1e-3), 1),
                        "x_c_only_GBps": round(rate(2 * (xb + cb), pair_ms), 1)},
         "codec_pair_projected": {
-            "ops": "compress_projected+decompress (tables built once per basis)",
+            "ops": "compress_projected+decompress, back to back (tables built once per basis)",
             "ms": round(ppair_ms, 5), "GBps": round(rate(ppair_bytes, ppair_ms), 1),
             "frac_hbm": round(rate(ppair_bytes, ppair_ms) / HBM_PEAK_GBS, 4),
             "tokens_per_s": round(N / (ppair_ms * 1e-3), 1),

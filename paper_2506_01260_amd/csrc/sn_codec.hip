@@ -104,13 +104,17 @@ struct RowSet {
   const bf16_t *ptr[R / 4];
 };
 
-template <int R>
+// STREAM: non-temporal copy (cache-policy bit 1), for rows read exactly once
+// (X): it keeps them from evicting the gathered rows, which are reused.
+template <int R, bool STREAM = false>
 __device__ __forceinline__ void dma_rows(const RowSet<R> &rs, int64_t col, u32x4 *dst, int q,
                                          int m) {
 #pragma unroll
   for (int i = 0; i < R / 4; ++i) {
     const int r = 4 * i + q;
-    lds_dma_16(rs.ptr[i] + col + 8 * (m ^ (r & 7)), dst + i * 64);
+    __builtin_amdgcn_global_load_lds(
+        static_cast<const void *>(rs.ptr[i] + col + 8 * (m ^ (r & 7))),
+        (__attribute__((address_space(3))) void *)(dst + i * 64), 16, 0, STREAM ? 2 : 0);
   }
 }
 
@@ -194,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const bf16_t *__rest
       u32x4 *b = lds + (si % NB) * G::buf_units;
       const int st = phys(si);
       const int64_t col = static_cast<int64_t>(st) * kStageCols;
-      dma_rows(pr.x, col, b + G::x_off, q, m);
+      dma_rows<kTokens, true>(pr.x, col, b + G::x_off, q, m);
       if (HE) dma_rows(pr.e, col, b + G::e_off, q, m);
       if (HP) dma_rows(pr.p, col, b + G::p_off, q, m);
       dma_frags(kfrag + static_cast<int64_t>(st) * 4 * KT * 512, 4 * KT, b + G::u_off, lane);
