@@ -27,6 +27,13 @@ constexpr int kBlock = 64 * kWaves;
 //          columns of one row: 16-byte stores) and B = rfrag.
 // W is read only by pass 1 and written only by pass 3 (stream order), so the
 // update is in place.
+//
+// When m is a multiple of 256 and k <= 64, pass 3 is the decompress kernel
+// instead: W = U T_hi + U T_lo = [U | U] [T_hi ; T_lo] is a decompress of the
+// d x 2k "coefficients" [U | U] against the m x 2k "basis" [T_hi | T_lo]^T,
+// which pass 2 then writes in the decompress operand layout (rfrag), together
+// with [U | U].  That kernel keeps its 256-column slice of the basis in LDS
+// and writes whole 256-byte row pieces.
 
 namespace {
 
@@ -37,20 +44,22 @@ struct ProjPlan {
   int64_t m_pad;      // m rounded up to kProjCols
   int kp;             // 16 * kt: fp32 row length of Tp
   int kp32;           // 32 * ks: bf16 row length of Th / Tl
+  int ks2;            // ceil(2k / 32): k-steps of [T_hi | T_lo]
   int dsplit;         // row splits in pass 1
   int64_t rows_per_split;
-  size_t off_tp, off_th, off_tl, total;
+  size_t off_tp, off_th, off_tl, off_tr, off_uu, total;
 };
 
 // Pass 1 splits the rows of W into dsplit ranges when there are too few
 // column slabs to fill the chip; it picks the split that minimises
 // (rounds of workgroups) x (rows per workgroup) for `slots` resident
 // workgroups (slots <= 0: the largest split, for the workspace bound).
-ProjPlan proj_plan(int64_t d, int kt, int ks, int64_t m, int64_t slots) {
+ProjPlan proj_plan(int64_t d, int64_t k, int kt, int ks, int64_t m, int64_t slots) {
   ProjPlan P;
   P.m_pad = ceil_div(m, kPadCols) * kPadCols;
   P.kp = 16 * kt;
   P.kp32 = 32 * ks;
+  P.ks2 = static_cast<int>(ceil_div(2 * k, 32));
   const int64_t slabs = ceil_div(m, 16 * (kt <= 4 ? 8 : 4));  // pass-1 workgroups per split
   int64_t max_ds = d / 128;  // >= 32 rows per wave
   if (max_ds > 8) max_ds = 8;
@@ -75,6 +84,10 @@ ProjPlan proj_plan(int64_t d, int kt, int ks, int64_t m, int64_t slots) {
   off = align256(off + static_cast<size_t>(P.m_pad) * P.kp32 * 2);
   P.off_tl = off;
   off = align256(off + static_cast<size_t>(P.m_pad) * P.kp32 * 2);
+  P.off_tr = off;  // [T_hi | T_lo] in the rfrag layout: m_pad x 32 ks2 bf16
+  off = align256(off + static_cast<size_t>(P.m_pad) * 32 * P.ks2 * 2);
+  P.off_uu = off;  // [U | U], d x 32 ks2 bf16
+  off = align256(off + static_cast<size_t>(d) * 32 * P.ks2 * 2);
   P.total = off;
   return P;
 }
@@ -225,6 +238,42 @@ __global__ __launch_bounds__(256) void project_pass2_kernel(const float *__restr
   Tl[idx] = lo;
 }
 
+// pass 2 for the decompress-form pass 3: one thread per (column c, j2) of
+// [T_hi | T_lo] (j2 < 32 ks2) and per (row r, j2) of [U | U].
+__global__ __launch_bounds__(256) void project_pass2_rfrag_kernel(
+    const float *__restrict__ Tp, int dsplit, int64_t m, int64_t m_pad, int kp, int64_t k,
+    int ks2, const float *__restrict__ Uf, int64_t d, bf16_t *__restrict__ tr,
+    bf16_t *__restrict__ uu) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int kp2 = 32 * ks2;
+  const int64_t nt = m * kp2;
+  if (idx < nt) {
+    const int64_t c = idx / kp2;
+    const int j2 = static_cast<int>(idx - c * kp2);
+    bf16_t out = bf16_t(0);
+    if (j2 < 2 * k) {
+      const int j = static_cast<int>(j2 < k ? j2 : j2 - k);
+      Dot2 acc;
+      for (int sp = 0; sp < dsplit; ++sp) acc.add(Tp[(sp * m_pad + c) * kp + j]);
+      const float v = acc.value();
+      const bf16_t hi = from_f32<bf16_t>(v);
+      out = j2 < k ? hi : from_f32<bf16_t>(v - to_f32(hi));
+    }
+    // rfrag slot of basis row c, k-index j2 (same layout as the packed basis)
+    const int64_t p = c / 32;
+    const int rr = static_cast<int>(c - 32 * p);
+    const int h = (rr >> 2) & 1, mm = 4 * (rr >> 3) + (rr & 3);
+    const int q = j2 >> 5, g = (j2 & 31) >> 3, e = j2 & 7;
+    tr[(((p * 2 + h) * ks2 + q) * 64 + 16 * g + mm) * 8 + e] = out;
+    return;
+  }
+  const int64_t i2 = idx - nt;
+  if (i2 >= d * kp2) return;
+  const int64_t r = i2 / kp2;
+  const int j2 = static_cast<int>(i2 - r * kp2);
+  uu[i2] = j2 < 2 * k ? from_f32<bf16_t>(Uf[r * k + (j2 < k ? j2 : j2 - k)]) : bf16_t(0);
+}
+
 template <int KS>
 __global__ __launch_bounds__(kBlock) void project_pass3_kernel(
     const bf16_t *__restrict__ rfrag, int64_t d, const bf16_t *__restrict__ Th,
@@ -359,7 +408,7 @@ int64_t pass1_slots(int kt) {
 
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m) {
   const int kt = static_cast<int>(ceil_div(k, 16)), ks = static_cast<int>(ceil_div(k, 32));
-  return proj_plan(d, kt, ks, m, 0).total;  // the largest split bounds every plan
+  return proj_plan(d, k, kt, ks, m, 0).total;  // the largest split bounds every plan
 }
 
 bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw) {
@@ -368,7 +417,7 @@ bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw)
 
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s) {
-  const ProjPlan P = proj_plan(L.d, L.kt, L.ks, m, pass1_slots(L.kt));
+  const ProjPlan P = proj_plan(L.d, L.k, L.kt, L.ks, m, pass1_slots(L.kt));
   const char *base = static_cast<const char *>(packed);
   const bf16_t *kf = reinterpret_cast<const bf16_t *>(base + L.off_kfrag);
   const bf16_t *rf = reinterpret_cast<const bf16_t *>(base + L.off_rfrag);
@@ -387,6 +436,26 @@ hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv
     case 7: launch_p1<7>(P, kf, L.d, W, m, ldw, Tp, s); break;
     case 8: launch_p1<8>(P, kf, L.d, W, m, ldw, Tp, s); break;
     default: return hipErrorNotSupported;
+  }
+  if (L.k <= 64 && m % 256 == 0) {
+    // pass 3 as a decompress of [U | U] against [T_hi | T_lo]
+    bf16_t *tr = reinterpret_cast<bf16_t *>(w + P.off_tr);
+    bf16_t *uu = reinterpret_cast<bf16_t *>(w + P.off_uu);
+    const int64_t n2 = (m + L.d) * 32 * P.ks2;
+    project_pass2_rfrag_kernel<<<dim3(static_cast<unsigned>(ceil_div(n2, 256))), 256, 0, s>>>(
+        Tp, P.dsplit, m, P.m_pad, P.kp, L.k, P.ks2,
+        reinterpret_cast<const float *>(base + L.off_f32), L.d, tr, uu);
+    PackLayout V;  // the m x 2k "basis" [T_hi | T_lo]^T, rfrag section only
+    V.d = m;
+    V.k = 2 * L.k;
+    V.dt = 1;
+    V.mfma = true;
+    V.kt = static_cast<int>(ceil_div(V.k, 16));
+    V.ks = P.ks2;
+    V.off_rfrag = P.off_tr;
+    IdArgs none{};
+    const hipError_t e = launch_decompress_mfma(V, ws, uu, L.d, 32 * P.ks2, none, W, ldw, s);
+    return e != hipSuccess ? e : hipGetLastError();
   }
   const int64_t n2 = P.m_pad * P.kp32;
   project_pass2_kernel<<<dim3(static_cast<unsigned>(ceil_div(n2, 256))), 256, 0, s>>>(
