@@ -30,6 +30,11 @@ PackLayout pack_layout(int64_t d, int64_t k, int dt) {
     off = align256(off + static_cast<size_t>(d / 32) * L.kt * 1024);
     L.off_rfrag = off;
     off = align256(off + static_cast<size_t>(d / 32) * 2 * L.ks * 1024);
+    if (k <= 64) {
+      L.ks2 = static_cast<int>(ceil_div(2 * k, 32));
+      L.off_uu = off;
+      off = align256(off + static_cast<size_t>(d) * 32 * L.ks2 * 2);
+    }
   }
   L.total = off;
   return L;
@@ -85,6 +90,18 @@ __global__ __launch_bounds__(256) void pack_rfrag_kernel(const bf16_t *__restric
   }
 }
 
+// [U | U] with zero columns up to 32 ks2, one thread per element.
+__global__ __launch_bounds__(256) void pack_uu_kernel(const bf16_t *__restrict__ U, int64_t d,
+                                                      int64_t k, int64_t ldu, int ks2,
+                                                      bf16_t *__restrict__ out) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int w = 32 * ks2;
+  if (idx >= d * w) return;
+  const int64_t r = idx / w;
+  const int64_t j = idx - r * w;
+  out[idx] = j < 2 * k ? U[r * ldu + (j < k ? j : j - k)] : bf16_t(0);
+}
+
 hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *packed,
                        hipStream_t s) {
   char *base = static_cast<char *>(packed);
@@ -104,6 +121,11 @@ hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *pa
     slots = (L.d / 32) * 2 * L.ks * 64;
     pack_rfrag_kernel<<<dim3(static_cast<unsigned>(ceil_div(slots, 256))), 256, 0, s>>>(
         Ub, L.d, L.k, ldu, L.ks, reinterpret_cast<bf16_t *>(base + L.off_rfrag));
+    if (L.ks2 > 0) {
+      const int64_t nu = L.d * 32 * L.ks2;
+      pack_uu_kernel<<<dim3(static_cast<unsigned>(ceil_div(nu, 256))), 256, 0, s>>>(
+          Ub, L.d, L.k, ldu, L.ks2, reinterpret_cast<bf16_t *>(base + L.off_uu));
+    }
   }
   return hipGetLastError();
 }

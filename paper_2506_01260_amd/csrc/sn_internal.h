@@ -28,13 +28,17 @@ inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 //        l = 16 g + m holds the 8 bf16 U[32 p + 8 (m/4) + 4 h + m%4, 32 q + 8 g + e].
 //        The row order puts 8 consecutive d-rows of one token in one lane of
 //        the MFMA result, so decompress stores 16 bytes per lane.
+//  uu    (same condition and k <= 64) [U | U] as bf16, d x 32 ceil(2k/32),
+//        columns past 2k zero: the coefficients of the weight projection's
+//        second contraction written as a decompress.
 struct PackLayout {
   int64_t d = 0, k = 0;
   int dt = 0;
   bool mfma = false;
   int kt = 0;   // ceil(k/16)
   int ks = 0;   // ceil(k/32)
-  size_t off_f32 = 0, off_kfrag = 0, off_rfrag = 0, total = 0;
+  int ks2 = 0;  // ceil(2k/32) when the uu section exists, else 0
+  size_t off_f32 = 0, off_kfrag = 0, off_rfrag = 0, off_uu = 0, total = 0;
 };
 
 PackLayout pack_layout(int64_t d, int64_t k, int dt);

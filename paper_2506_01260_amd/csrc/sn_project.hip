@@ -30,10 +30,10 @@ constexpr int kBlock = 64 * kWaves;
 //
 // When m is a multiple of 256 and k <= 64, pass 3 is the decompress kernel
 // instead: W = U T_hi + U T_lo = [U | U] [T_hi ; T_lo] is a decompress of the
-// d x 2k "coefficients" [U | U] against the m x 2k "basis" [T_hi | T_lo]^T,
-// which pass 2 then writes in the decompress operand layout (rfrag), together
-// with [U | U].  That kernel keeps its 256-column slice of the basis in LDS
-// and writes whole 256-byte row pieces.
+// d x 2k "coefficients" [U | U] (a section of the packed basis) against the
+// m x 2k "basis" [T_hi | T_lo]^T, which pass 2 then writes in the decompress
+// operand layout (rfrag).  That kernel keeps its 256-column slice of the
+// basis in LDS and writes whole 256-byte row pieces.
 
 namespace {
 
@@ -47,14 +47,14 @@ struct ProjPlan {
   int ks2;            // ceil(2k / 32): k-steps of [T_hi | T_lo]
   int dsplit;         // row splits in pass 1
   int64_t rows_per_split;
-  size_t off_tp, off_th, off_tl, off_tr, off_uu, total;
+  size_t off_tp, off_th, off_tl, off_tr, total;
 };
 
 // Pass 1 splits the rows of W into dsplit ranges when there are too few
 // column slabs to fill the chip; it picks the split that minimises
 // (rounds of workgroups) x (rows per workgroup) for `slots` resident
 // workgroups (slots <= 0: the largest split, for the workspace bound).
-ProjPlan proj_plan(int64_t d, int64_t k, int kt, int ks, int64_t m, int64_t slots) {
+ProjPlan proj_plan(int64_t k, int kt, int ks, int64_t m, int64_t d, int64_t slots) {
   ProjPlan P;
   P.m_pad = ceil_div(m, kPadCols) * kPadCols;
   P.kp = 16 * kt;
@@ -86,8 +86,6 @@ ProjPlan proj_plan(int64_t d, int64_t k, int kt, int ks, int64_t m, int64_t slot
   off = align256(off + static_cast<size_t>(P.m_pad) * P.kp32 * 2);
   P.off_tr = off;  // [T_hi | T_lo] in the rfrag layout: m_pad x 32 ks2 bf16
   off = align256(off + static_cast<size_t>(P.m_pad) * 32 * P.ks2 * 2);
-  P.off_uu = off;  // [U | U], d x 32 ks2 bf16
-  off = align256(off + static_cast<size_t>(d) * 32 * P.ks2 * 2);
   P.total = off;
   return P;
 }
@@ -238,40 +236,41 @@ __global__ __launch_bounds__(256) void project_pass2_kernel(const float *__restr
   Tl[idx] = lo;
 }
 
-// pass 2 for the decompress-form pass 3: one thread per (column c, j2) of
-// [T_hi | T_lo] (j2 < 32 ks2) and per (row r, j2) of [U | U].
+// pass 2 for the decompress-form pass 3: one thread per (column c, j) with
+// j < 16 ks2; for j < k it writes T_hi[j, c] and T_lo[j, c] (k-indices j and
+// k + j of [T_hi | T_lo]), past k two of the zero pad entries.
 __global__ __launch_bounds__(256) void project_pass2_rfrag_kernel(
     const float *__restrict__ Tp, int dsplit, int64_t m, int64_t m_pad, int kp, int64_t k,
-    int ks2, const float *__restrict__ Uf, int64_t d, bf16_t *__restrict__ tr,
-    bf16_t *__restrict__ uu) {
+    int ks2, bf16_t *__restrict__ tr) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  const int kp2 = 32 * ks2;
-  const int64_t nt = m * kp2;
-  if (idx < nt) {
-    const int64_t c = idx / kp2;
-    const int j2 = static_cast<int>(idx - c * kp2);
-    bf16_t out = bf16_t(0);
-    if (j2 < 2 * k) {
-      const int j = static_cast<int>(j2 < k ? j2 : j2 - k);
-      Dot2 acc;
-      for (int sp = 0; sp < dsplit; ++sp) acc.add(Tp[(sp * m_pad + c) * kp + j]);
-      const float v = acc.value();
-      const bf16_t hi = from_f32<bf16_t>(v);
-      out = j2 < k ? hi : from_f32<bf16_t>(v - to_f32(hi));
-    }
-    // rfrag slot of basis row c, k-index j2 (same layout as the packed basis)
-    const int64_t p = c / 32;
-    const int rr = static_cast<int>(c - 32 * p);
-    const int h = (rr >> 2) & 1, mm = 4 * (rr >> 3) + (rr & 3);
-    const int q = j2 >> 5, g = (j2 & 31) >> 3, e = j2 & 7;
-    tr[(((p * 2 + h) * ks2 + q) * 64 + 16 * g + mm) * 8 + e] = out;
-    return;
+  const int half = 16 * ks2;
+  if (idx >= m * half) return;
+  const int64_t c = idx / half;
+  const int j = static_cast<int>(idx - c * half);
+  bf16_t v0 = bf16_t(0), v1 = bf16_t(0);
+  int j0, j1;
+  if (j < k) {
+    Dot2 acc;
+    for (int sp = 0; sp < dsplit; ++sp) acc.add(Tp[(sp * m_pad + c) * kp + j]);
+    const float v = acc.value();
+    v0 = from_f32<bf16_t>(v);
+    v1 = from_f32<bf16_t>(v - to_f32(v0));
+    j0 = j;
+    j1 = static_cast<int>(k) + j;
+  } else {
+    j0 = static_cast<int>(2 * k + 2 * (j - k));
+    j1 = j0 + 1;
   }
-  const int64_t i2 = idx - nt;
-  if (i2 >= d * kp2) return;
-  const int64_t r = i2 / kp2;
-  const int j2 = static_cast<int>(i2 - r * kp2);
-  uu[i2] = j2 < 2 * k ? from_f32<bf16_t>(Uf[r * k + (j2 < k ? j2 : j2 - k)]) : bf16_t(0);
+  // rfrag slot of basis row c, k-index j2 (the packed-basis rfrag layout)
+  const int64_t p = c / 32;
+  const int rr = static_cast<int>(c - 32 * p);
+  const int h = (rr >> 2) & 1, mm = 4 * (rr >> 3) + (rr & 3);
+  auto put = [&](int j2, bf16_t x) {
+    const int q = j2 >> 5, g = (j2 & 31) >> 3, e = j2 & 7;
+    tr[(((p * 2 + h) * ks2 + q) * 64 + 16 * g + mm) * 8 + e] = x;
+  };
+  put(j0, v0);
+  put(j1, v1);
 }
 
 template <int KS>
@@ -408,7 +407,7 @@ int64_t pass1_slots(int kt) {
 
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m) {
   const int kt = static_cast<int>(ceil_div(k, 16)), ks = static_cast<int>(ceil_div(k, 32));
-  return proj_plan(d, k, kt, ks, m, 0).total;  // the largest split bounds every plan
+  return proj_plan(k, kt, ks, m, d, 0).total;  // the largest split bounds every plan
 }
 
 bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw) {
@@ -417,7 +416,7 @@ bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw)
 
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s) {
-  const ProjPlan P = proj_plan(L.d, L.k, L.kt, L.ks, m, pass1_slots(L.kt));
+  const ProjPlan P = proj_plan(L.k, L.kt, L.ks, m, L.d, pass1_slots(L.kt));
   const char *base = static_cast<const char *>(packed);
   const bf16_t *kf = reinterpret_cast<const bf16_t *>(base + L.off_kfrag);
   const bf16_t *rf = reinterpret_cast<const bf16_t *>(base + L.off_rfrag);
@@ -437,14 +436,13 @@ hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv
     case 8: launch_p1<8>(P, kf, L.d, W, m, ldw, Tp, s); break;
     default: return hipErrorNotSupported;
   }
-  if (L.k <= 64 && m % 256 == 0) {
+  if (L.ks2 > 0 && m % 256 == 0) {
     // pass 3 as a decompress of [U | U] against [T_hi | T_lo]
     bf16_t *tr = reinterpret_cast<bf16_t *>(w + P.off_tr);
-    bf16_t *uu = reinterpret_cast<bf16_t *>(w + P.off_uu);
-    const int64_t n2 = (m + L.d) * 32 * P.ks2;
+    const bf16_t *uu = reinterpret_cast<const bf16_t *>(base + L.off_uu);
+    const int64_t n2 = m * 16 * P.ks2;
     project_pass2_rfrag_kernel<<<dim3(static_cast<unsigned>(ceil_div(n2, 256))), 256, 0, s>>>(
-        Tp, P.dsplit, m, P.m_pad, P.kp, L.k, P.ks2,
-        reinterpret_cast<const float *>(base + L.off_f32), L.d, tr, uu);
+        Tp, P.dsplit, m, P.m_pad, P.kp, L.k, P.ks2, tr);
     PackLayout V;  // the m x 2k "basis" [T_hi | T_lo]^T, rfrag section only
     V.d = m;
     V.k = 2 * L.k;
