@@ -63,6 +63,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--rotate", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the configs 1, 3 and 4 timings and the copy reference")
     ap.add_argument("--cpu-rows", type=int, default=32768,
                     help="tokens in the oracle's timed sample")
     ap.add_argument("--profile-pass", action="store_true",
@@ -281,6 +283,153 @@ def trace_summary(trace_dir: str, bench_log: str):
                             "ms_per_step": b["ms_per_step"], "roofline": b["roofline"],
                             "codec_pair": b["codec_pair"]}) + "\n```\n")
     print(open(out).read())
+
+
+def _pair_times(sn, torch, basis, d, k, tok, E, P, seq, steps, R=2, grad=True):
+    """Back-to-back compress+decompress (and grad compress+decompress) over R
+    rotating buffer sets of device-drawn inputs; mean ms per pair."""
+    N = tok.shape[0]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(N * 7 + d)
+    Xs = [torch.randn(N, d, device="cuda", generator=gen).to(torch.bfloat16) for _ in range(R)]
+    Cs = [torch.empty(N, k, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    Os = [torch.empty(N, d, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    stream = torch.cuda.current_stream()
+
+    def loop(fn):
+        for i in range(3):
+            fn(i % R)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(steps):
+            fn(i % R)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    def fwd(j):
+        sn.sn_compress(basis, Xs[j], tok=tok, E=E, P=P, seq_len=seq, out=Cs[j])
+        sn.sn_decompress(basis, Cs[j], tok=tok, E=E, P=P, seq_len=seq, out=Os[j])
+
+    def bwd(j):
+        sn.sn_grad_compress(basis, Xs[j], out=Cs[j])
+        sn.sn_decompress(basis, Cs[j], out=Os[j])
+
+    out = {"pair_ms": loop(fwd)}
+    if grad:
+        out["grad_pair_ms"] = loop(bwd)
+    del Xs, Cs, Os
+    return out
+
+
+def other_configs(sn, torch, steps: int) -> dict:
+    """The forward and gradient pairs at configs 1 and 4 (N = 32768 and the
+    ragged 32767), the config-4 Wo projection, the config-3 sweep of 32 x
+    (Wo, W2), and a plain device copy for reference.  U and the ids are the
+    configs' own; E, P, X and the weights are drawn on the device with the
+    configs' shapes and scales (timing does not depend on the values)."""
+    import synth
+    res = {}
+
+    def rate(nbytes, ms):
+        return nbytes / (ms * 1e-3) / 1e9
+
+    for cid, ns in ((1, (None,)), (4, (None, 32767))):
+        cfg = synth.CONFIGS[cid]
+        d, k = cfg.d, cfg.k
+        U = to_dev(synth.make_basis(cid)["U"])
+        basis = sn.sn_basis_pack(U)
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(synth.seed_of(cid, synth.ORD_E))
+        E = (torch.randn(cfg.vocab, d, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+        P = (torch.randn(cfg.seq, d, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+        entry = {}
+        for n in ns:
+            ids = synth.make_ids(cid, n)
+            tok = torch.from_numpy(ids["tok"]).cuda()
+            N = tok.shape[0]
+            t = _pair_times(sn, torch, basis, d, k, tok, E, P, cfg.seq, steps)
+            uniq = len(np.unique(ids["tok"])) * d * 2 + min(cfg.seq, N) * d * 2
+            pair_bytes = 2 * (N * d * 2 + N * k * 2 + uniq + d * k * 2)
+            grad_bytes = 2 * (N * d * 2 + N * k * 2 + d * k * 2)
+            entry[f"N{N}"] = {
+                "pair_ms": round(t["pair_ms"], 5),
+                "pair_GBps": round(rate(pair_bytes, t["pair_ms"]), 1),
+                "pair_frac_hbm": round(rate(pair_bytes, t["pair_ms"]) / HBM_PEAK_GBS, 4),
+                "pair_tokens_per_s": round(N / (t["pair_ms"] * 1e-3), 1),
+                "grad_pair_ms": round(t["grad_pair_ms"], 5),
+                "grad_pair_GBps": round(rate(grad_bytes, t["grad_pair_ms"]), 1)}
+        for i, (rows, cols) in enumerate(cfg.weights if cid == 4 else ()):
+            ws = torch.empty(sn.sn_project_weights_workspace_bytes(d, k, sn.SN_BF16, cols),
+                             dtype=torch.uint8, device="cuda")
+            Wl = [synth.device_weight(cid, i, rows, cols) for _ in range(2)]
+            for j in range(3):
+                sn.sn_project_weights(basis, Wl[j % 2], workspace=ws)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for j in range(steps):
+                sn.sn_project_weights(basis, Wl[j % 2], workspace=ws)
+            b.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b) / steps
+            entry[f"project_W{i}_ms"] = round(ms, 5)
+            entry[f"project_W{i}_GBps"] = round(rate(2 * rows * cols * 2, ms), 1)
+            del Wl, ws
+        res[f"cfg{cid}"] = {"d": d, "k": k, **entry}
+        del E, P, basis, U
+        torch.cuda.empty_cache()
+        print(f"[bench] config {cid} timed", file=sys.stderr, flush=True)
+
+    # config 3: one in-place sweep of 32 layers x (Wo, W2)
+    cfg = synth.CONFIGS[3]
+    U = to_dev(synth.make_basis(3)["U"])
+    basis = sn.sn_basis_pack(U)
+    mats = [synth.device_weight(3, 2 * layer + i, r, c)
+            for layer in range(cfg.layers) for i, (r, c) in enumerate(cfg.weights)]
+    ws = torch.empty(max(sn.sn_project_weights_workspace_bytes(cfg.d, cfg.k, sn.SN_BF16, c)
+                         for _, c in cfg.weights), dtype=torch.uint8, device="cuda")
+
+    def sweep():
+        for Wm in mats:
+            sn.sn_project_weights(basis, Wm, workspace=ws)
+
+    sweep()
+    torch.cuda.synchronize()
+    reps = 3
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        sweep()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    nbytes = sum(2 * Wm.numel() * 2 for Wm in mats)
+    res["cfg3_sweep"] = {"matrices": len(mats), "ms": round(ms, 4),
+                         "GBps": round(rate(nbytes, ms), 1),
+                         "frac_hbm": round(rate(nbytes, ms) / HBM_PEAK_GBS, 4)}
+    del mats, ws, basis, U
+    torch.cuda.empty_cache()
+
+    # reference: a plain device-to-device copy of 1 GiB (reads and writes it)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / 5
+    res["device_copy"] = {"bytes_moved": 2 << 30, "ms": round(ms, 4),
+                          "GBps": round(rate(2 << 30, ms), 1)}
+    del src, dst
+    torch.cuda.empty_cache()
+    return res
 
 
 def load_traffic():
@@ -526,6 +675,10 @@ def main():
                      "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": dom_traffic,
                      "algorithmic_bytes": op_bytes[dom]},
     }
+    if not args.no_other_configs:
+        del Xs, Gs, Cs, Cgs, Cps, Xrs, Grs, weights
+        torch.cuda.empty_cache()
+        out["other_configs"] = other_configs(sn, torch, K)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         cb_ = cpu_baseline(w, host_weights, min(args.cpu_rows, N))

@@ -123,6 +123,17 @@ __device__ __forceinline__ void add8(float (&o)[8], u32x4 v) {
   }
 }
 
+// LDS of a workgroup besides the U slice: the per-wave transpose buffers and,
+// when there are tables, the staged ids (a union-free pair of layouts so the
+// kernels without tables stay within two workgroups per CU at ks = 3).
+struct DSmemIds {
+  f32x4 ot[kDW][16 * 32];
+  int2 idl[kDW][kMaxWaveTiles][16];  // (token id, position id) per tile row
+};
+struct DSmemPlain {
+  f32x4 ot[kDW][16 * 32];
+};
+
 template <int KS, bool HE, bool HP, int CM>
 __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     const bf16_t *__restrict__ rfrag, int64_t k, const bf16_t *__restrict__ C, int64_t ldc,
@@ -130,8 +141,8 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     int tiles_per_wg) {
   constexpr int FR = 2 * KS;  // fragments per row group
   __shared__ u32x4 us[kPG * FR * 64];
-  __shared__ f32x4 ot[kDW][16 * 32];
-  __shared__ int2 idl[kDW][kMaxWaveTiles][16];  // (token id, position id) per tile row
+  constexpr bool kIds = HE || HP;
+  __shared__ typename std::conditional<kIds, DSmemIds, DSmemPlain>::type sm;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -160,7 +171,8 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
 
   // Stage the ids of all the wave's tiles in LDS up front (fixed trip count,
   // clamped tiles: all loads are in flight before the first wait).
-  if (nt > 0) {
+  if constexpr (kIds) {
+    if (nt > 0) {
     int2 v[kMaxWaveTiles / 4];
 #pragma unroll
     for (int i = 0; i < kMaxWaveTiles / 4; ++i) {
@@ -178,7 +190,8 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
       }
     }
 #pragma unroll
-    for (int i = 0; i < kMaxWaveTiles / 4; ++i) idl[wave][4 * i + g][n] = v[i];
+    for (int i = 0; i < kMaxWaveTiles / 4; ++i) sm.idl[wave][4 * i + g][n] = v[i];
+    }
   }
   {  // the block's U slice -> LDS, 1 KiB per direct-to-LDS load
     const bf16_t *src = rfrag + static_cast<int64_t>(cb) * kPG * FR * 512;
@@ -189,7 +202,7 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   if (nt == 0) return;
 
   const int64_t col_r = static_cast<int64_t>(cb) * kDCols + 8 * m;  // row-layout column
-  f32x4 *otw = ot[wave];
+  f32x4 *otw = sm.ot[wave];
   int bad = 0;
 
   auto load_tile = [&](DTile<KS> &dt, int j) {
@@ -199,9 +212,11 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     for (int i = 0; i < 4; ++i) {
       const int r = 4 * i + q;
       const int t = token(T, r);
-      const int2 v = idl[wave][j < nt ? j : nt - 1][r];
-      if (HE) dt.er[i] = static_cast<int>(clamp_flag(v.x, ids.vocab, 1, bad));
-      if (HP) dt.pr[i] = static_cast<int>(clamp_flag(v.y, ids.n_pos, 2, bad));
+      if constexpr (kIds) {
+        const int2 v = sm.idl[wave][j < nt ? j : nt - 1][r];
+        if (HE) dt.er[i] = static_cast<int>(clamp_flag(v.x, ids.vocab, 1, bad));
+        if (HP) dt.pr[i] = static_cast<int>(clamp_flag(v.y, ids.n_pos, 2, bad));
+      }
       dt.xr[i] = t;
     }
   };
@@ -303,13 +318,28 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   if (bad && ids.err_flag) atomicOr(ids.err_flag, bad);
 }
 
+// Resident workgroups of a kernel on the current device (CUs x occupancy).
+template <typename K>
+int64_t resident_slots(K kernel) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(kernel),
+                                                   kDThreads, 0) != hipSuccess ||
+      cus <= 0 || per_cu <= 0)
+    return 512;
+  return static_cast<int64_t>(cus) * per_cu;
+}
+
 template <int KS, bool HE, bool HP, int CM>
 void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
                 const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
   const int ncb = static_cast<int>(L.d / kDCols);
   const int64_t ntiles = ceil_div(tm.N, 16);
-  // about two resident workgroups per CU over the whole grid, whole waves of tiles
-  int64_t per = ceil_div(ntiles * ncb, 512);
+  // one round of resident workgroups over the whole grid, whole waves of tiles
+  static const int64_t slots = resident_slots(decompress_cb_kernel<KS, HE, HP, CM>);
+  const int64_t groups = slots / ncb > 0 ? slots / ncb : 1;  // token groups per round
+  int64_t per = ceil_div(ntiles, groups);
   per = per < kDW ? kDW : (per > kDW * kMaxWaveTiles ? kDW * kMaxWaveTiles : per);
   per = ceil_div(per, kDW) * kDW;
   const int64_t tgroups = ceil_div(ntiles, per);
