@@ -8,23 +8,26 @@
 //            is exact and every sum is fp32.
 // Without tables this is the gradient compress of Sec. 4.4.
 //
-// compress_kernel (one workgroup = 4 compute waves + 1 producer wave, 64 tokens):
+// compress_kernel (one workgroup = 4 compute waves + 3 producer waves, 64 tokens):
 //
-// * The producer wave copies, for each stage of 128 columns of d, everything
+// * Three producer waves copy, for each stage of 64 columns of d, everything
 //   the compute waves need into one of NB LDS buffers with direct-to-LDS
-//   loads: the 64 tokens' X rows, their E and P rows, and the U fragments of
-//   the stage.  Each copy instruction reads 4 rows x 256 contiguous bytes
-//   (contiguous row pieces are much cheaper for the memory pipeline than the
-//   16-rows-x-64-bytes pattern of an MFMA operand), and the 16-byte pieces of
-//   row r are stored in the order p ^ (r & 7) so that the compute waves'
-//   operand reads (16 rows, same piece) hit distinct banks.
+//   loads: wave A the 64 tokens' X rows, wave B their T_fixed and P rows,
+//   wave C the U fragments of the stage.  Each copy instruction reads 8 rows
+//   x 128 contiguous bytes (contiguous row pieces are much cheaper for the
+//   memory pipeline than the 16-rows-x-64-bytes pattern of an MFMA operand),
+//   and the 16-byte pieces of row r are stored in the order p ^ (r & 7) so
+//   that the compute waves' operand reads (16 rows, same piece) spread over
+//   the banks.
 // * Compute wave w owns 16 tokens and the whole of d; it reads operands only
 //   from LDS (no global loads in its main loop), so nothing stalls it but the
 //   hand-over barrier.
-// * NB-deep buffering: the producer keeps NB-1 stages in flight; one barrier
-//   per stage hands a buffer over.  Workgroups start at different stages
-//   (rotation) so the rows in flight across the chip are not read at the same
-//   column offsets.
+// * NB-deep buffering (NB = 6 at k <= 48): the copies keep NB - 1 stages in
+//   flight, which is what sets the kernel's speed (one workgroup per CU);
+//   three producers keep each wave's outstanding copies within the 6-bit
+//   vmcnt range.  One barrier per stage hands a buffer over.  Workgroups
+//   start at different stages (rotation) so the rows in flight across the
+//   chip are not read at the same column offsets.
 // * Position-major tiles (positions i mod seq_len, batch a multiple of 4): a
 //   16-token tile holds 16/B consecutive positions of B batches, so the tile
 //   needs only 16/B positional rows.
@@ -40,8 +43,12 @@ namespace {
 constexpr int kW = 4;                  // compute waves per workgroup
 constexpr int kThreads = 64 * (kW + 1);
 constexpr int kTokens = 16 * kW;       // tokens per workgroup
-constexpr int kStageCols = 128;        // d-elements per stage
-constexpr int kPieces = 16;            // 16-byte pieces per row per stage
+constexpr int kStageCols = 64;         // d-elements per stage
+constexpr int kPieces = 8;             // 16-byte pieces per row per stage
+constexpr int kRowsPerCopy = 64 / kPieces;  // rows per direct-to-LDS copy instruction
+constexpr int kProd = 3;               // producer waves of compress_kernel
+constexpr int kThreadsC = 64 * (kW + kProd);
+constexpr int kMaxStages = 6;
 constexpr int kLdsBytes = 160 * 1024;
 
 // 16-byte LDS slot of piece p of row r in a row tile.
@@ -86,22 +93,31 @@ struct CGeo {
   static constexpr int e_off = x_off + kTokens * kPieces;
   static constexpr int p_off = e_off + (HE ? kTokens * kPieces : 0);
   static constexpr int u_off = p_off + (HP ? p_rows<PM>() * kPieces : 0);
-  static constexpr int buf_units = u_off + 4 * KT * 64;
-  static constexpr int dma_per_stage = kTokens / 4 + (HE ? kTokens / 4 : 0) +
-                                       (HP ? p_rows<PM>() / 4 : 0) + 4 * KT;
-  static constexpr int nb =
-      (3 * buf_units * 16 <= kLdsBytes && dma_per_stage <= 63) ? 3 : 2;
-  static_assert(nb * buf_units * 16 <= kLdsBytes, "stage buffers exceed LDS");
+  static constexpr int u_frags = (kStageCols / 32) * KT;
+  static constexpr int buf_units = u_off + u_frags * 64;
+  // copy instructions per stage of each producer: X; gathered rows; U
+  static constexpr int dma_a = kTokens / kRowsPerCopy;
+  static constexpr int dma_b =
+      (HE ? kTokens / kRowsPerCopy : 0) + (HP ? p_rows<PM>() / kRowsPerCopy : 0);
+  static constexpr int dma_c = u_frags;
+  static constexpr int dmax = dma_a > dma_b ? (dma_a > dma_c ? dma_a : dma_c)
+                                            : (dma_b > dma_c ? dma_b : dma_c);
+  // as many stages as LDS holds (at most kMaxStages), with (nb - 2) stages of
+  // every producer's copies countable by vmcnt
+  static constexpr int nb_lds = kLdsBytes / (buf_units * 16);
+  static constexpr int nb_cap = nb_lds < kMaxStages ? nb_lds : kMaxStages;
+  static constexpr int nb = nb_cap - 2 > 63 / dmax ? 2 + 63 / dmax : nb_cap;
+  static_assert(nb >= 3, "at least two stages in flight");
 };
 
 // ---------------------------------------------------------------------------
-// Producer wave
+// Producer waves
 // ---------------------------------------------------------------------------
-// Row pointers of the rows this lane copies: row r = 4 i + q of a tile of R
-// rows (q = lane / 16); lane (q, m) copies piece m ^ (r & 7) of row r.
+// Row pointers of the rows this lane copies: row r = 8 i + q of a tile of R
+// rows (q = lane / 8); lane (q, m) copies piece m ^ (r & 7) of row r.
 template <int R>
 struct RowSet {
-  const bf16_t *ptr[R / 4];
+  const bf16_t *ptr[R / kRowsPerCopy];
 };
 
 // STREAM: non-temporal copy (cache-policy bit 1), for rows read exactly once
@@ -110,8 +126,8 @@ template <int R, bool STREAM = false>
 __device__ __forceinline__ void dma_rows(const RowSet<R> &rs, int64_t col, u32x4 *dst, int q,
                                          int m) {
 #pragma unroll
-  for (int i = 0; i < R / 4; ++i) {
-    const int r = 4 * i + q;
+  for (int i = 0; i < R / kRowsPerCopy; ++i) {
+    const int r = kRowsPerCopy * i + q;
     __builtin_amdgcn_global_load_lds(
         static_cast<const void *>(rs.ptr[i] + col + 8 * (m ^ (r & 7))),
         (__attribute__((address_space(3))) void *)(dst + i * 64), 16, 0, STREAM ? 2 : 0);
@@ -127,57 +143,31 @@ __device__ __forceinline__ const bf16_t *row_ptr(const void *base, int64_t ld, i
   return static_cast<const bf16_t *>(base) + row * ld;
 }
 
-// The producer's rows for the workgroup's 64 tokens (tiles T0..T0+3).
-template <bool WITH_X, bool HE, bool HP, bool PM>
-struct ProducerRows {
-  RowSet<kTokens> x, e;
-  RowSet<p_rows<PM>()> p;
-
-  __device__ void init(const Tiling &tm, int64_t T0, int64_t ntiles, const bf16_t *X,
-                       int64_t ldx, const IdArgs &ids, int q) {
-#pragma unroll
-    for (int i = 0; i < kTokens / 4; ++i) {
-      const int r = 4 * i + q;  // token row r = 16 w + n
-      int64_t T = T0 + r / 16;
-      T = T < ntiles ? T : ntiles - 1;
-      const int64_t t = tile_token(tm, T, r % 16);
-      if (WITH_X) x.ptr[i] = X + t * ldx;
-      if (HE) {
-        const int64_t id = clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1);
-        e.ptr[i] = row_ptr(ids.E, ids.lde, id);
-      }
-      if (HP && !PM) {
-        int64_t ps = ids.pos ? static_cast<int64_t>(ids.pos[t]) : t % ids.seq_len;
-        ps = clamp_id(ps, ids.n_pos, ids.err_flag, 2);
-        p.ptr[i] = row_ptr(ids.P, ids.ldp, ps);
-      }
+// Wait until at most `later` stages of PER copies each are outstanding
+// (later <= L, a compile-time bound: vmcnt takes an immediate).
+template <int PER, int L>
+__device__ __forceinline__ void wait_stages(int later) {
+  if constexpr (L > 0) {
+    if (later >= L) {
+      wait_vmcnt<L * PER>();
+      return;
     }
-    if (HP && PM) {
-      // positional row r = w * pg + rho of the workgroup (rows past 4 pg repeat
-      // the last one so the copy count stays fixed)
-      const int pg = 16 / tm.bp;
-#pragma unroll
-      for (int i = 0; i < p_rows<PM>() / 4; ++i) {
-        int r = 4 * i + q;
-        r = r < kW * pg ? r : kW * pg - 1;
-        int64_t T = T0 + r / pg;
-        T = T < ntiles ? T : ntiles - 1;
-        p.ptr[i] = row_ptr(ids.P, ids.ldp, tile_pos0(tm, T) + r % pg);
-      }
-    }
+    wait_stages<PER, L - 1>(later);
+  } else {
+    wait_vmcnt<0>();
   }
-};
+}
 
 // ---------------------------------------------------------------------------
 // compress
 // ---------------------------------------------------------------------------
 template <int KT, bool HE, bool HP, bool PM>
-__global__ __launch_bounds__(kThreads) void compress_kernel(const bf16_t *__restrict__ kfrag,
-                                                            int64_t d, int64_t k,
-                                                            const bf16_t *__restrict__ X,
-                                                            int64_t ldx, Tiling tm, IdArgs ids,
-                                                            bf16_t *__restrict__ C, int64_t ldc,
-                                                            int cvec) {
+__global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__restrict__ kfrag,
+                                                             int64_t d, int64_t k,
+                                                             const bf16_t *__restrict__ X,
+                                                             int64_t ldx, Tiling tm, IdArgs ids,
+                                                             bf16_t *__restrict__ C,
+                                                             int64_t ldc, int cvec) {
   using G = CGeo<KT, HE, HP, PM>;
   constexpr int NB = G::nb;
   __shared__ u32x4 lds[NB * G::buf_units];
@@ -190,32 +180,72 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const bf16_t *__rest
   const int64_t ntiles = (tm.N + 15) / 16;
   const int64_t T0 = static_cast<int64_t>(blockIdx.x) * kW;
 
-  if (wave == kW) {  // ------------------------------------------------ producer
-    const int q = lane >> 4, m = lane & 15;
-    ProducerRows<true, HE, HP, PM> pr;
-    pr.init(tm, T0, ntiles, X, ldx, ids, q);
+  if (wave >= kW) {  // ------------------------------------------------ producers
+    const int role = wave - kW;  // 0: X rows, 1: T_fixed and P rows, 2: U fragments
+    const int q = lane / kPieces, m = lane % kPieces;
+    RowSet<kTokens> rx, re;
+    RowSet<p_rows<PM>()> rp;
+    // token row r = 16 w + n of the workgroup (tiles past the end repeat the last)
+    auto token_of = [&](int r) {
+      int64_t T = T0 + r / 16;
+      T = T < ntiles ? T : ntiles - 1;
+      return tile_token(tm, T, r % 16);
+    };
+    if (role == 0) {
+#pragma unroll
+      for (int i = 0; i < kTokens / kRowsPerCopy; ++i)
+        rx.ptr[i] = X + token_of(kRowsPerCopy * i + q) * ldx;
+    } else if (role == 1) {
+#pragma unroll
+      for (int i = 0; i < kTokens / kRowsPerCopy; ++i) {
+        const int64_t t = token_of(kRowsPerCopy * i + q);
+        if (HE) re.ptr[i] = row_ptr(ids.E, ids.lde, clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1));
+        if (HP && !PM) {
+          int64_t ps = ids.pos ? static_cast<int64_t>(ids.pos[t]) : t % ids.seq_len;
+          ps = clamp_id(ps, ids.n_pos, ids.err_flag, 2);
+          rp.ptr[i] = row_ptr(ids.P, ids.ldp, ps);
+        }
+      }
+      if (HP && PM) {
+        // positional row r = w * pg + rho of the workgroup (rows past 4 pg
+        // repeat the last one so the copy count stays fixed)
+        const int pg = 16 / tm.bp;
+#pragma unroll
+        for (int i = 0; i < p_rows<PM>() / kRowsPerCopy; ++i) {
+          int r = kRowsPerCopy * i + q;
+          r = r < kW * pg ? r : kW * pg - 1;
+          int64_t T = T0 + r / pg;
+          T = T < ntiles ? T : ntiles - 1;
+          rp.ptr[i] = row_ptr(ids.P, ids.ldp, tile_pos0(tm, T) + r % pg);
+        }
+      }
+    }
     auto issue = [&](int si) {
       u32x4 *b = lds + (si % NB) * G::buf_units;
       const int st = phys(si);
       const int64_t col = static_cast<int64_t>(st) * kStageCols;
-      dma_rows<kTokens, true>(pr.x, col, b + G::x_off, q, m);
-      if (HE) dma_rows(pr.e, col, b + G::e_off, q, m);
-      if (HP) dma_rows(pr.p, col, b + G::p_off, q, m);
-      dma_frags(kfrag + static_cast<int64_t>(st) * 4 * KT * 512, 4 * KT, b + G::u_off, lane);
+      if (role == 0) {
+        dma_rows<kTokens, true>(rx, col, b + G::x_off, q, m);
+      } else if (role == 1) {
+        if (HE) dma_rows(re, col, b + G::e_off, q, m);
+        if (HP) dma_rows(rp, col, b + G::p_off, q, m);
+      } else {
+        dma_frags(kfrag + static_cast<int64_t>(st) * G::u_frags * 512, G::u_frags, b + G::u_off,
+                  lane);
+      }
     };
-#pragma unroll
     for (int s = 0; s < NB - 1; ++s)
       if (s < nst) issue(s);
     for (int s = 0; s < nst; ++s) {
-      // stage s has landed once at most the later in-flight stage is pending
-      if constexpr (NB == 3) {
-        if (s + 1 < nst)
-          wait_vmcnt<G::dma_per_stage>();
-        else
-          wait_vmcnt<0>();
-      } else {
-        wait_vmcnt<0>();
-      }
+      // stage s has landed once at most the later stages in flight are pending
+      int later = nst - 1 - s;
+      later = later < NB - 2 ? later : NB - 2;
+      if (role == 0)
+        wait_stages<G::dma_a, NB - 2>(later);
+      else if (role == 1)
+        wait_stages<G::dma_b, NB - 2>(later);
+      else
+        wait_stages<G::dma_c, NB - 2>(later);
       lds_barrier();
       if (s + NB - 1 < nst) issue(s + NB - 1);
     }
@@ -235,7 +265,7 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const bf16_t *__rest
     lds_barrier();  // stage s is in buffer s % NB
     const u32x4 *b = lds + (s % NB) * G::buf_units;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kStageCols / 32; ++j) {
       const int pc = 4 * j + g;
       const u32x4 bx = b[G::x_off + slot(xrow, pc)];
       u32x4 be, bpv;
@@ -460,7 +490,7 @@ void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx,
               const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s) {
   const int64_t ntiles = (tm.N + 15) / 16;
   dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
-  compress_kernel<KT, HE, HP, PM><<<grid, kThreads, 0, s>>>(
+  compress_kernel<KT, HE, HP, PM><<<grid, kThreadsC, 0, s>>>(
       kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, static_cast<bf16_t *>(C), ldc,
       cvec);
 }
