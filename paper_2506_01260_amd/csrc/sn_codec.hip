@@ -161,13 +161,20 @@ __device__ __forceinline__ void wait_stages(int later) {
 // ---------------------------------------------------------------------------
 // compress
 // ---------------------------------------------------------------------------
-template <int KT, bool HE, bool HP, bool PM>
+// Epilogues: bf16 coefficients; coefficients against projected tables
+// (C = X U - (P U)[pos] - (T_fixed U)[tok], the subtraction done on the k
+// coefficients of each token); fp32 rows of a projected table (padded to
+// 16 ceil(k/16) columns, zero past k).
+enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2 };
+
+template <int KT, bool HE, bool HP, bool PM, int EPI>
 __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__restrict__ kfrag,
                                                              int64_t d, int64_t k,
                                                              const bf16_t *__restrict__ X,
                                                              int64_t ldx, Tiling tm, IdArgs ids,
-                                                             bf16_t *__restrict__ C,
+                                                             ProjArgs pa, void *__restrict__ Cout,
                                                              int64_t ldc, int cvec) {
+  static_assert(EPI == kEpiBf16 || (!HE && !HP && !PM), "projected epilogues have no tables");
   using G = CGeo<KT, HE, HP, PM>;
   constexpr int NB = G::nb;
   __shared__ u32x4 lds[NB * G::buf_units];
@@ -287,11 +294,31 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
   const int64_t i = 16 * T + n;
   const int64_t tok = tm.bp == 1 ? i : tile_token(tm, T, n);
   if (tm.bp == 1 && i >= tm.N) return;
+  if (EPI == kEpiProjected) {
+    // C = X U - (P U)[pos] - (T_fixed U)[tok], in the paper's order
+    if (pa.pu) {
+      int64_t ps = pa.pos ? static_cast<int64_t>(pa.pos[tok]) : tok % pa.seq_len;
+      ps = clamp_id(ps, pa.n_pos, pa.err_flag, 2);
+      const float *pr = pa.pu + ps * pa.kp + 4 * g;
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[t] -= *reinterpret_cast<const f32x4 *>(pr + 16 * t);
+    }
+    if (pa.eu) {
+      const int64_t tk = clamp_id(pa.tok[tok], pa.vocab, pa.err_flag, 1);
+      const float *er = pa.eu + tk * pa.kp + 4 * g;
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[t] -= *reinterpret_cast<const f32x4 *>(er + 16 * t);
+    }
+  }
 #pragma unroll
   for (int t = 0; t < KT; ++t) {
     const f32x4 v = acc[t];
     const int64_t j = 16 * t + 4 * g;
-    bf16_t *dst = C + tok * ldc + j;
+    if (EPI == kEpiF32) {  // full padded row of the projected table (columns >= k are 0)
+      *reinterpret_cast<f32x4 *>(static_cast<float *>(Cout) + tok * ldc + j) = v;
+      continue;
+    }
+    bf16_t *dst = static_cast<bf16_t *>(Cout) + tok * ldc + j;
     if (cvec && j + 4 <= k) {
       *reinterpret_cast<u32x2 *>(dst) = u32x2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
     } else {
@@ -315,7 +342,6 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
 // buffers (one barrier per chunk).  The ring loads are unconditional (the
 // loads past the end re-read the last step) and pinned in place, so the
 // compiler keeps all D in flight.
-enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2 };
 
 template <int KT>
 constexpr int s_chunk_steps() { return KT <= 4 ? 8 : 4; }
@@ -485,14 +511,46 @@ Tiling pick_tiling(int64_t N, const IdArgs &ids) {
   return tm;
 }
 
-template <int KT, bool HE, bool HP, bool PM>
+template <int KT, bool HE, bool HP, bool PM, int EPI = kEpiBf16>
 void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx, const Tiling &tm,
-              const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s) {
+              const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s,
+              const ProjArgs &pa = ProjArgs{}) {
   const int64_t ntiles = (tm.N + 15) / 16;
   dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
-  compress_kernel<KT, HE, HP, PM><<<grid, kThreadsC, 0, s>>>(
-      kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, static_cast<bf16_t *>(C), ldc,
-      cvec);
+  compress_kernel<KT, HE, HP, PM, EPI><<<grid, kThreadsC, 0, s>>>(
+      kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec);
+}
+
+// X U with no gathered rows, on the staged kernel (d a multiple of kStageCols)
+template <int EPI>
+hipError_t launch_plain_kt(const PackLayout &L, const void *packed, const void *X, int64_t N,
+                           int64_t ldx, const ProjArgs &pa, void *C, int64_t ldc, hipStream_t s) {
+  const bf16_t *kf =
+      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_kfrag);
+  const int cvec = ((reinterpret_cast<uintptr_t>(C) & 7) == 0) && (ldc % 4 == 0);
+  const Tiling tm{N, 1, 1};
+  const IdArgs none{};
+  switch (L.kt) {
+    case 1: launch_c<1, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 2: launch_c<2, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 3: launch_c<3, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 4: launch_c<4, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 5: launch_c<5, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 6: launch_c<6, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 7: launch_c<7, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 8: launch_c<8, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+// X U with no gathered rows: the staged kernel when d allows, else the
+// register-ring streaming kernel
+template <int EPI>
+hipError_t launch_plain(const PackLayout &L, const void *packed, const void *X, int64_t N,
+                        int64_t ldx, const ProjArgs &pa, void *C, int64_t ldc, hipStream_t s) {
+  if (L.d % kStageCols == 0) return launch_plain_kt<EPI>(L, packed, X, N, ldx, pa, C, ldc, s);
+  return launch_stream_kt<EPI>(L, packed, X, N, ldx, pa, C, ldc, s);
 }
 
 template <int KT>
@@ -527,7 +585,7 @@ hipError_t launch_compress_mfma(const PackLayout &L, const void *packed, const v
   const bf16_t *kf =
       reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_kfrag);
   const int cvec = ((reinterpret_cast<uintptr_t>(C) & 7) == 0) && (ldc % 4 == 0);
-  if (!ids.E && !ids.P) return launch_stream_kt<kEpiBf16>(L, packed, X, N, ldx, ProjArgs{}, C, ldc, s);
+  if (!ids.E && !ids.P) return launch_plain<kEpiBf16>(L, packed, X, N, ldx, ProjArgs{}, C, ldc, s);
   const Tiling tm = pick_tiling(N, ids);
   switch (L.kt) {
     case 1: launch_c_kt<1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
@@ -550,13 +608,13 @@ bool stream_mfma_ok(const PackLayout &L, const void *X, int64_t ldx) {
 hipError_t launch_table_project_mfma(const PackLayout &L, const void *packed, const void *T,
                                      int64_t rows, int64_t ldt, float *out, int64_t kp,
                                      hipStream_t s) {
-  return launch_stream_kt<kEpiF32>(L, packed, T, rows, ldt, ProjArgs{}, out, kp, s);
+  return launch_plain<kEpiF32>(L, packed, T, rows, ldt, ProjArgs{}, out, kp, s);
 }
 
 hipError_t launch_compress_projected_mfma(const PackLayout &L, const void *packed, const void *X,
                                           int64_t N, int64_t ldx, const ProjArgs &pa, void *C,
                                           int64_t ldc, hipStream_t s) {
-  return launch_stream_kt<kEpiProjected>(L, packed, X, N, ldx, pa, C, ldc, s);
+  return launch_plain<kEpiProjected>(L, packed, X, N, ldx, pa, C, ldc, s);
 }
 
 }  // namespace sn
