@@ -48,11 +48,11 @@ CALIB_BYTES = 256 * 1024 * 1024   # plain copy used to scale the HBM counters
 
 # rocprofv3 kernel names of each op (substring match on the demangled name)
 OP_KERNELS = {
-    "compress": ["compress_kernel<3, true, true, true>"],
+    "compress": ["compress_kernel<3, true, true, true, 0>"],
     "decompress": ["decompress_cb_kernel<2, true, true, 0>"],
-    "grad_compress": ["stream_compress_kernel<3, 0>"],
+    "grad_compress": ["compress_kernel<3, false, false, false, 0>"],
     "grad_decompress": ["decompress_cb_kernel<2, false, false, 0>"],
-    "compress_projected": ["stream_compress_kernel<3, 1>"],
+    "compress_projected": ["compress_kernel<3, false, false, false, 1>"],
 }
 
 
@@ -238,14 +238,19 @@ def trace_summary(trace_dir: str, bench_log: str):
             ("timed steps", s0 + W * per_step, s0 + (W + K) * per_step),
             ("timed steps, event per op", s0 + (W + K) * per_step, s0 + (W + 2 * K) * per_step)]
     e = cuts[-1][2]
+    e2 = e + 2 * pair
+    proj = OP_KERNELS["compress_projected"][0]
+    tb_end = next((i for i in range(e2, len(rows)) if proj in rows[i]["Kernel_Name"]), None)
+    if tb_end is None or tb_end + K > len(rows):
+        raise SystemExit("dispatch count does not match the bench's phase layout")
     cuts += [("compress+decompress loop, warm-up", e, e + 6),
              ("compress+decompress loop, timed", e + 6, e + pair),
              ("compress_projected+decompress loop, warm-up", e + pair, e + pair + 6),
-             ("compress_projected+decompress loop, timed", e + pair + 6, e + 2 * pair),
-             ("table build", e + 2 * pair, len(rows) - K),
-             ("compress_projected alone", len(rows) - K, len(rows))]
-    if cuts[-1][1] < cuts[-2][1]:
-        raise SystemExit("dispatch count does not match the bench's phase layout")
+             ("compress_projected+decompress loop, timed", e + pair + 6, e2),
+             ("table build", e2, tb_end),
+             ("compress_projected alone", tb_end, tb_end + K)]
+    if tb_end + K < len(rows):
+        cuts.append(("other configs (1, 4, 3-layer sweep; warm-up included)", tb_end + K, len(rows)))
     out = os.path.join(ROOT, "profiles", "codec_step_d4096_k40_kernel_stats.md")
     with open(out, "w") as f:
         f.write("# Kernel durations: codec step at d=4096, k=40, N=32768 (bf16)\n\n")
