@@ -63,6 +63,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--rotate", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured in a HIP graph and replayed (the "
+                         "replays measured no faster than eager launches here)")
     ap.add_argument("--no-other-configs", action="store_true",
                     help="skip the configs 1, 3 and 4 timings and the copy reference")
     ap.add_argument("--cpu-rows", type=int, default=32768,
@@ -94,10 +97,14 @@ def to_dev(a, bf16=True):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def cpu_baseline(w, weights, rows: int):
+def cpu_baseline(w, weights, rows: int, step_bytes: int, min_seconds: float = 10.0,
+                 max_reps: int = 5):
     """The oracle, as it stands, on a bounded sample of the same step: the
     first `rows` tokens through compress, decompress, grad compress and grad
-    decompress, plus the projection of every weight matrix of the step."""
+    decompress, plus the projection of every weight matrix of the step,
+    repeated until about `min_seconds` of CPU work (at most `max_reps`
+    times).  The rate is in the bench's unit: the sample's share of the
+    step's algorithmic bytes per second (tokens/s alongside)."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -112,20 +119,30 @@ def cpu_baseline(w, weights, rows: int):
     tok = w["tok"][:rows]
     Ws = [dec(Wb) for Wb in weights]
     t0 = time.perf_counter()
-    C = oracle.round_bf16(oracle.compress(X, U, tok, E, P, seq_len=cfg.seq))
-    oracle.round_bf16(oracle.decompress(C, U, tok, E, P, seq_len=cfg.seq))
-    Cg = oracle.round_bf16(oracle.grad_compress(G, U))
-    oracle.round_bf16(oracle.grad_decompress(Cg, U))
-    for Wf in Ws:
-        oracle.round_bf16(oracle.project_weights(Wf, U))
-    dt = time.perf_counter() - t0
+    reps = 0
+    while True:
+        C = oracle.round_bf16(oracle.compress(X, U, tok, E, P, seq_len=cfg.seq))
+        oracle.round_bf16(oracle.decompress(C, U, tok, E, P, seq_len=cfg.seq))
+        Cg = oracle.round_bf16(oracle.grad_compress(G, U))
+        oracle.round_bf16(oracle.grad_decompress(Cg, U))
+        for Wf in Ws:
+            oracle.round_bf16(oracle.project_weights(Wf, U))
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds or reps >= max_reps:
+            break
     frac = rows / cfg.n_tokens
-    return {"value": rows / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    # bytes of the sample: the token-proportional part of the step scaled by
+    # the sample fraction (the weights are always whole)
+    wbytes = sum(2 * Wf.size * 2 for Wf in Ws)
+    sample_bytes = (step_bytes - wbytes) * frac + wbytes
+    return {"value": round(sample_bytes * reps / dt / 1e9, 3), "unit": "GB/s",
+            "tokens_per_s": round(rows * reps / dt, 1), "cores": int(threads), "kind": "oracle",
             "sample": f"{rows} of {cfg.n_tokens} tokens through compress, decompress, grad "
-                      f"compress and grad decompress, plus the projection of Wo and W2 "
-                      f"({dt:.2f} s of CPU time; the sample is {frac:.0%} of the step's tokens "
-                      f"and all of its weights)",
-            "seconds": dt}
+                      f"compress and grad decompress, plus the projection of Wo and W2, "
+                      f"{reps} time(s) ({dt:.2f} s of CPU time; the sample is {frac:.0%} of the "
+                      f"step's tokens and all of its weights)",
+            "seconds": round(dt, 3), "repetitions": reps}
 
 
 # --------------------------------------------------------------------------- counters
@@ -233,10 +250,16 @@ def trace_summary(trace_dir: str, bench_log: str):
     starts = [i for i, n in enumerate(names) if n == comp]
     s0, per_step = starts[0], starts[1] - starts[0]
     pair = 2 * (3 + K)
+    R = b["config"].get("rotate_buffers", 3)
     cuts = [("set-up", 0, s0),
             ("warm-up steps", s0, s0 + W * per_step),
-            ("timed steps", s0 + W * per_step, s0 + (W + K) * per_step),
-            ("timed steps, event per op", s0 + (W + K) * per_step, s0 + (W + 2 * K) * per_step)]
+            ("timed steps", s0 + W * per_step, s0 + (W + K) * per_step)]
+    at = s0 + (W + K) * per_step
+    if b.get("graph_replay_ms_per_step") is not None:
+        cuts += [("graph replays, warm-up", at, at + 2 * R * per_step),
+                 ("timed graph replays", at + 2 * R * per_step, at + (2 * R + K) * per_step)]
+        at += (2 * R + K) * per_step
+    cuts.append(("timed steps, event per op", at, at + K * per_step))
     e = cuts[-1][2]
     e2 = e + 2 * pair
     proj = OP_KERNELS["compress_projected"][0]
@@ -563,7 +586,7 @@ def main():
 
     K = args.steps
     mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))  # noqa: E731
-    # the step time: K steps with events only at the two ends
+    # eager step time: K steps with events only at the two ends
     t_start, t_end = mk()
     torch.cuda.synchronize()
     t_start.record(stream)
@@ -571,9 +594,36 @@ def main():
         step(args.warmup + i)
     t_end.record(stream)
     torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_step = total_ms / K
-    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+    eager_ms = t_start.elapsed_time(t_end) / K
+    print(f"[bench] timed {K} eager steps: {eager_ms:.4f} ms/step", file=sys.stderr, flush=True)
+    # optionally: the same step captured once per buffer set in a HIP graph
+    # (every launch of the step, nothing else) and replayed K times
+    ms_step = eager_ms
+    graph_ms = None
+    if args.graph:
+        graphs = []
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            for j in range(R):
+                gr = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gr, stream=cap):
+                    step(j)
+                graphs.append(gr)
+        stream.wait_stream(cap)
+        for i in range(2 * R):
+            graphs[i % R].replay()
+        torch.cuda.synchronize()
+        t_start, t_end = mk()
+        t_start.record(stream)
+        for i in range(K):
+            graphs[(args.warmup + i) % R].replay()
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = t_start.elapsed_time(t_end) / K
+        print(f"[bench] timed {K} graph replays: {graph_ms:.4f} ms/step", file=sys.stderr,
+              flush=True)
+        del graphs
     # per-op times: K more steps with an event pair around every launch (the
     # marker packets add a few microseconds per op, so these sum to more than
     # the step time above)
@@ -648,6 +698,7 @@ def main():
         "steps": K,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
+        "graph_replay_ms_per_step": None if graph_ms is None else round(graph_ms, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -686,7 +737,7 @@ def main():
         out["other_configs"] = other_configs(sn, torch, K)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        cb_ = cpu_baseline(w, host_weights, min(args.cpu_rows, N))
+        cb_ = cpu_baseline(w, host_weights, min(args.cpu_rows, N), step_bytes)
         out["cpu_baseline"] = {kk: (round(v, 3) if isinstance(v, float) else v)
                                for kk, v in cb_.items()}
     print(json.dumps(out), flush=True)
