@@ -15,13 +15,17 @@ the output dtype with round-to-nearest-even:
 * ``project_weights`` W' = U (U^T W)                              (Sec. 4.3 / Sec. 5: rows of the
   projection matrices confined to S = Col(U); Appendix E's projection Pi_S)
 
+The subspace update of Section 4.5 (off-subspace loss, accumulation matrix,
+Riemannian gradient, QR retraction) is in ``grassmann``.
+
 ``exact`` holds the same operations in exact rational arithmetic
 (``fractions.Fraction``) for brute-force checks on tiny inputs.
 """
 from .bf16 import decode_bf16, encode_bf16, round_bf16, round_f32, round_to
 from .codec import (compress, decompress, grad_compress, grad_decompress,
                     project_weights, default_positions)
+from . import grassmann
 
 __all__ = ["decode_bf16", "encode_bf16", "round_bf16", "round_f32", "round_to",
            "compress", "decompress", "grad_compress", "grad_decompress",
-           "project_weights", "default_positions"]
+           "project_weights", "default_positions", "grassmann"]

@@ -6,7 +6,8 @@ projection routine and nothing here is ever used to produce an expected value.
 
 Every tensor is drawn on the host with numpy ``Generator(PCG64(seed))`` where
 ``seed = 1260 + 100 * cfg + ordinal`` (ordinal: 0 U, 1 E, 2 P, 3 tok,
-4 C_true, 5 noise, 6 G, 7 + i weight matrix i).  Large tensors are drawn in
+4 C_true, 5 noise, 6 G, 7 + i weight matrix i, 79 the dominant gradient
+directions and 80 + t the gradient of iteration t of the subspace update).  Large tensors are drawn in
 fixed row blocks of ``ROW_BLOCK`` rows, block b using ``SeedSequence([seed, b])``,
 so a tensor's values do not depend on how callers slice it.
 
@@ -63,6 +64,8 @@ CONFIGS = {
 }
 
 ORD_U, ORD_E, ORD_P, ORD_TOK, ORD_C, ORD_NOISE, ORD_G, ORD_W = range(8)
+ORD_GV = 79        # fixed dominant gradient directions of the subspace-update inputs
+ORD_GT = 80        # 80 + t: activation gradient of accumulated iteration t (t < 20)
 
 
 def seed_of(cfg: int, ordinal: int) -> int:
@@ -248,6 +251,41 @@ def make_gradient(cfg_id: int, n: int | None = None, cfg: Config | None = None) 
     cfg = cfg or CONFIGS[cfg_id]
     n = cfg.n_tokens if n is None else n
     return store(gaussian(seed_of(cfg_id, ORD_G), n, cfg.d, cfg.g_std), cfg.dtype)
+
+
+def make_grad_iteration(cfg_id: int, t: int, n: int | None = None, cfg: Config | None = None,
+                        rank: int | None = None, share: float = 0.5) -> np.ndarray:
+    """Activation gradient of accumulated iteration t for the subspace update
+    (Section 4.5): rows g = g_std (a z V^T + b e) with V (d x rank) a fixed
+    orthonormal set of dominant directions, z ~ N(0, I_rank), e ~ N(0, I_d),
+    a^2 = share d / rank and b^2 = 1 - share, so a fraction `share` of each
+    row's expected energy d g_std^2 lies in span(V).  Gradients concentrated
+    in a few directions give the update something to align U with."""
+    cfg = cfg or CONFIGS[cfg_id]
+    if not 0 <= t < 20:
+        raise ValueError("t must be in [0, 20)")
+    n = cfg.n_tokens if n is None else n
+    rank = cfg.k if rank is None else rank
+    ft = np.float64 if cfg.dtype == "f32" else np.float32
+    V = orthonormal_basis(seed_of(cfg_id, ORD_GV), cfg.d, rank).astype(ft)
+    a = ft((share * cfg.d / rank) ** 0.5)
+    b = ft((1.0 - share) ** 0.5)
+    out = np.empty((n, cfg.d), dtype=np.float32 if cfg.dtype == "f32" else np.uint16)
+    seed = seed_of(cfg_id, ORD_GT + t)
+
+    def one(item):
+        blk_i, r0 = item
+        r1 = min(n, r0 + ROW_BLOCK)
+        rng = _rng(seed, blk_i)
+        z = rng.standard_normal((r1 - r0, rank), dtype=ft)
+        e = rng.standard_normal((r1 - r0, cfg.d), dtype=ft)
+        g = (a * z) @ V.T
+        g += b * e
+        g *= ft(cfg.g_std)
+        out[r0:r1] = store(g, cfg.dtype)
+
+    _parallel(one, _blocks(n))
+    return out
 
 
 def make_weight(cfg_id: int, index: int, rows: int, cols: int,
