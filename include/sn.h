@@ -214,6 +214,88 @@ int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt,
                            void *workspace, size_t workspace_bytes, sn_stream stream);
 
 /* ------------------------------------------------------------------------ */
+/* Subspace update (Sec. 4.5; cost analysis of Sec. 6).                        */
+/*                                                                            */
+/* Between two updates the last compressed layer's activation gradients G_t   */
+/* (N x d) are accumulated for K iterations; the update then takes one step   */
+/* on the Grassmann manifold against                                          */
+/*   L = (1/K) sum_t |G_t (I - U U^T)|_F^2        (the off-subspace loss)     */
+/* with Euclidean gradient -2 S U, S = (1/K) sum_t G_t^T G_t, projected onto  */
+/* the tangent space, followed by a QR retraction.                            */
+/*                                                                            */
+/* Because U is fixed between updates, S U = (1/K) sum_t G_t^T (G_t U): the   */
+/* state keeps the d x k matrix Y = sum_t G_t^T (G_t U) instead of the d x d  */
+/* S, and each iteration costs one more pass over G instead of a d x d        */
+/* product.  k <= 128.                                                        */
+/*                                                                            */
+/* State buffer (device, 256-byte aligned, sn_grassmann_state_bytes bytes),   */
+/* float64:                                                                   */
+/*   [0] sum over accumulated iterations of |G_t (I - U U^T)|_F^2             */
+/*   [1] K_L, the number of iterations in [0]                                 */
+/*   [2] L = [0] / [1] (the loss of Sec. 4.5; 0 before the first iteration)   */
+/*   [3] K_S, the number of iterations accumulated into Y                     */
+/*   Y   d x k (row stride k) at byte offset 256                              */
+/* The loss uses U exactly as stored: with a bf16 basis U^T U is not exactly  */
+/* I, and the row term |g|^2 - 2 |g U|^2 + (g U)(U^T U)(g U)^T is evaluated   */
+/* with that U.                                                               */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of the accumulator state for a d x k basis (0 if invalid or k > 128). */
+size_t sn_grassmann_state_bytes(int64_t d, int64_t k);
+
+/* Workspace bytes of sn_grassmann_accumulate with N tokens; with N = 0, of
+ * sn_grassmann_step.  A buffer of the size for the largest N serves both.
+ * 0 if invalid. */
+size_t sn_grassmann_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t N);
+
+/* Zero the state (start of an accumulation interval).  Launched as a kernel
+ * (no memset), so it may be captured in a graph.  Errors: NULL, ALIGN, SHAPE,
+ * UNSUPPORTED, HIP. */
+int32_t sn_grassmann_reset(void *state, int64_t d, int64_t k, sn_stream stream);
+
+/* sn_grassmann_accumulate: one iteration's contribution.
+ *
+ *   basis      packed basis of (d, k, dt); U must be the basis the step will use
+ *   G          N x d activation gradient (row stride ldg >= d), dt
+ *   Cg         N x k output (row stride ldc >= k), or NULL: when given, receives
+ *              the gradient coefficients G U exactly as sn_grad_compress writes
+ *              them, so one call serves as the gradient codec and the update's
+ *              accumulation
+ *   with_su    nonzero: also Y += G^T (G U) and K_S += 1; zero: only the loss
+ *              (the residual monitor)
+ *   state      accumulator (see above), updated in place
+ *   workspace  sn_grassmann_workspace_bytes(d, k, dt, N) bytes, 256-byte aligned
+ * Adds |G (I - U U^T)|_F^2 to [0], 1 to [1] and rewrites [2].  N == 0 is a
+ * no-op.  No buffer may overlap another.  Errors: NULL, SHAPE, DTYPE, ALIGN,
+ * ALIAS, WORKSPACE, UNSUPPORTED, HIP. */
+int32_t sn_grassmann_accumulate(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                const void *G, int64_t N, int64_t ldg,
+                                void *Cg, int64_t ldc, int32_t with_su,
+                                void *state, void *workspace, size_t workspace_bytes,
+                                sn_stream stream);
+
+/* sn_grassmann_step: U_new = Q of the thin QR (diag(R) > 0) of U - eta T,
+ * T = G_E - U U^T G_E the Riemannian gradient of L, G_E = -2 S U = -(2/K_S) Y.
+ *
+ *   basis      packed basis of the current U (d x k, dt)
+ *   state      accumulated by sn_grassmann_accumulate with this basis; read only
+ *              (K_S = 0 gives T = 0: U_new is U re-orthonormalised)
+ *   eta        step size, finite and >= 0
+ *   U_new      d x k output, row stride ldu >= k, element type out_dt (rounded
+ *              once from float64); pack it with sn_basis_pack to use it
+ *   workspace  sn_grassmann_workspace_bytes(d, k, dt, 0) bytes, 256-byte aligned
+ *   err_flag   device int32 or NULL: bit 2 is set when U - eta T is numerically
+ *              rank deficient, in which case U_new receives U unchanged
+ * The weights confined to the old subspace are re-confined to the new one with
+ * sn_project_weights.  Errors: NULL, SHAPE, DTYPE, ALIGN, ALIAS, WORKSPACE,
+ * UNSUPPORTED, HIP. */
+int32_t sn_grassmann_step(const void *basis, int64_t d, int64_t k, int32_t dt,
+                          const void *state, double eta,
+                          void *U_new, int64_t ldu, int32_t out_dt,
+                          void *workspace, size_t workspace_bytes, int32_t *err_flag,
+                          sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics.                                                               */
 /* ------------------------------------------------------------------------ */
 

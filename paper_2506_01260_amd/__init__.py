@@ -15,6 +15,10 @@ built the first call raises ``RuntimeError``.
 
     proj = sn_embed_project(basis, E=E, P=P)         # T_fixed U, P U (once per basis)
     C  = sn_compress_projected(basis, X, proj, tok=tok, seq_len=S)
+
+    state = sn_grassmann_state(basis)                # subspace update (Sec. 4.5)
+    Cg = sn_grassmann_accumulate(basis, G, state, want_cg=True)   # per iteration
+    U2 = sn_grassmann_step(basis, state, eta)        # every few hundred iterations
 """
 from __future__ import annotations
 
@@ -54,6 +58,13 @@ _SIGNATURES = {
                                      _I64, _I64, _P, _I64, _P, _P]),
     "sn_project_weights_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
     "sn_project_weights": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _SZ, _P]),
+    "sn_grassmann_state_bytes": (_SZ, [_I64, _I64]),
+    "sn_grassmann_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
+    "sn_grassmann_reset": (_I32, [_P, _I64, _I64, _P]),
+    "sn_grassmann_accumulate": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _I64, _I32, _P,
+                                       _P, _SZ, _P]),
+    "sn_grassmann_step": (_I32, [_P, _I64, _I64, _I32, _P, ctypes.c_double, _P, _I64, _I32, _P,
+                                 _SZ, _P, _P]),
     "sn_status_string": (ctypes.c_char_p, [_I32]),
     "sn_last_error": (ctypes.c_char_p, []),
     "sn_version": (ctypes.c_char_p, []),
@@ -317,6 +328,104 @@ def sn_project_weights(basis: Basis, W: torch.Tensor, workspace=None, stream=Non
     _check(lib().sn_project_weights(basis.ptr, d, basis.k, basis.dt, wp, m, ldw,
                                     workspace.data_ptr(), workspace.numel(), _stream(stream)))
     return W
+
+
+class GrassmannState:
+    """Accumulator of the subspace update (one device buffer, see include/sn.h):
+    float64 [loss sum, K_L, L, K_S] and Y = sum_t G_t^T (G_t U) (d x k)."""
+
+    HEAD = 256
+
+    def __init__(self, buf: torch.Tensor, d: int, k: int):
+        self.buf, self.d, self.k = buf, d, k
+
+    @property
+    def ptr(self):
+        return self.buf.data_ptr()
+
+    def scalars(self) -> torch.Tensor:
+        """Device view of [loss sum, K_L, L, K_S] (float64)."""
+        return self.buf[:32].view(torch.float64)
+
+    def Y(self) -> torch.Tensor:
+        """Device view of Y (d x k, float64)."""
+        n = self.d * self.k * 8
+        return self.buf[self.HEAD:self.HEAD + n].view(torch.float64).view(self.d, self.k)
+
+
+def sn_grassmann_state_bytes(d: int, k: int) -> int:
+    return lib().sn_grassmann_state_bytes(d, k)
+
+
+def sn_grassmann_workspace_bytes(d: int, k: int, dt: int, N: int) -> int:
+    return lib().sn_grassmann_workspace_bytes(d, k, dt, N)
+
+
+def sn_grassmann_reset(state: GrassmannState, stream=None) -> GrassmannState:
+    _check(lib().sn_grassmann_reset(state.ptr, state.d, state.k, _stream(stream)))
+    return state
+
+
+def sn_grassmann_state(basis: Basis, device="cuda", stream=None) -> GrassmannState:
+    """A zeroed accumulator state for the basis's (d, k)."""
+    nbytes = sn_grassmann_state_bytes(basis.d, basis.k)
+    if nbytes == 0:
+        raise SnError(8, f"no subspace-update state for d = {basis.d}, k = {basis.k}")
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return sn_grassmann_reset(GrassmannState(buf, basis.d, basis.k), stream)
+
+
+def _grass_ws(basis: Basis, N: int, workspace, device):
+    need = sn_grassmann_workspace_bytes(basis.d, basis.k, basis.dt, N)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    if workspace.numel() < need or not workspace.is_cuda:
+        raise SnError(9, f"workspace needs {need} device bytes")
+    return workspace
+
+
+def sn_grassmann_accumulate(basis: Basis, G: torch.Tensor, state: GrassmannState,
+                            with_su: bool = True, want_cg: bool = False, out=None,
+                            workspace=None, stream=None):
+    """Add one iteration's gradient G (N x d) to the state: the off-subspace
+    loss always, Y += G^T (G U) when with_su.  With want_cg (or out given)
+    also returns the gradient coefficients G U as sn_grad_compress writes them."""
+    gp, N, d, ldg = _mat(G, "G")
+    _same_d(basis, d)
+    if (state.d, state.k) != (basis.d, basis.k):
+        raise SnError(2, "state was made for another basis shape")
+    if out is None and want_cg:
+        out = torch.empty((N, basis.k), dtype=_torch_dtype(basis.dt), device=G.device)
+    cp = ldc = 0
+    if out is not None:
+        _out_shape(out, (N, basis.k), "out")
+        _same_dtype(basis, ("out", out))
+        cp, _, _, ldc = _mat(out, "out")
+    _same_dtype(basis, ("G", G))
+    ws = _grass_ws(basis, N, workspace, G.device)
+    _check(lib().sn_grassmann_accumulate(basis.ptr, basis.d, basis.k, basis.dt, gp, N, ldg,
+                                         cp or None, ldc, 1 if with_su else 0, state.ptr,
+                                         ws.data_ptr(), ws.numel(), _stream(stream)))
+    return out
+
+
+def sn_grassmann_step(basis: Basis, state: GrassmannState, eta: float, out_dtype=None, out=None,
+                      workspace=None, err_flag=None, stream=None) -> torch.Tensor:
+    """U_new: one Riemannian gradient step of size eta on the accumulated loss,
+    retracted by QR (diag(R) > 0).  out_dtype defaults to the basis dtype."""
+    if (state.d, state.k) != (basis.d, basis.k):
+        raise SnError(2, "state was made for another basis shape")
+    tdt = out.dtype if out is not None else (out_dtype or _torch_dtype(basis.dt))
+    if out is None:
+        out = torch.empty((basis.d, basis.k), dtype=tdt, device=state.buf.device)
+    _out_shape(out, (basis.d, basis.k), "out")
+    up, _, _, ldu = _mat(out, "out")
+    ws = _grass_ws(basis, 0, workspace, state.buf.device)
+    _check(lib().sn_grassmann_step(basis.ptr, basis.d, basis.k, basis.dt, state.ptr, float(eta),
+                                   up, ldu, _dt(out), ws.data_ptr(), ws.numel(),
+                                   None if err_flag is None else err_flag.data_ptr(),
+                                   _stream(stream)))
+    return out
 
 
 def sn_version() -> str:

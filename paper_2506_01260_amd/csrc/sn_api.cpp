@@ -117,6 +117,32 @@ int32_t check_out_alias(Span out, const void *basis, size_t basis_bytes, Span in
   return SN_OK;
 }
 
+Span bytes_span(const void *p, size_t n) {
+  Span s;
+  if (!p || n == 0) return s;
+  s.lo = reinterpret_cast<uintptr_t>(p);
+  s.hi = s.lo + n;
+  return s;
+}
+
+int32_t check_state(const void *state, int64_t d, int64_t k) {
+  if (!state) return fail(SN_ERR_NULL, "state is NULL");
+  if (reinterpret_cast<uintptr_t>(state) & 255)
+    return fail(SN_ERR_ALIGN, "state must be 256-byte aligned");
+  if (k > sn::kGrassMaxK)
+    return fail(SN_ERR_UNSUPPORTED, "subspace update needs k <= %d", sn::kGrassMaxK);
+  (void)d;
+  return SN_OK;
+}
+
+int32_t check_workspace(const void *ws, size_t have, size_t need) {
+  if (!ws) return fail(SN_ERR_NULL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) & 255)
+    return fail(SN_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (have < need) return fail(SN_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", have, need);
+  return SN_OK;
+}
+
 sn::IdArgs make_ids(const int32_t *tok, const void *E, int64_t vocab, int64_t lde,
                     const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
                     int64_t seq_len, int32_t *err_flag) {
@@ -386,6 +412,86 @@ int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt, 
                       "sn_project_weights launch");
   return hip_status(sn::launch_project_generic(L, basis, W, m, ldw, workspace, s),
                     "sn_project_weights launch");
+}
+
+size_t sn_grassmann_state_bytes(int64_t d, int64_t k) {
+  if (d < 1 || d >= kMaxDim || k < 1 || k > d || k > sn::kGrassMaxK) return 0;
+  return sn::grass_state_bytes(d, k);
+}
+
+size_t sn_grassmann_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t N) {
+  if (!dtype_ok(dt) || d < 1 || d >= kMaxDim || k < 1 || k > d || k > sn::kGrassMaxK || N < 0 ||
+      N >= kMaxDim)
+    return 0;
+  return sn::grass_workspace_bytes(sn::pack_layout(d, k, dt), N);
+}
+
+int32_t sn_grassmann_reset(void *state, int64_t d, int64_t k, sn_stream stream) {
+  if (d < 1 || d >= kMaxDim || k < 1 || k > d) return fail(SN_ERR_SHAPE, "need 1 <= k <= d");
+  int32_t st = check_state(state, d, k);
+  if (st) return st;
+  return hip_status(sn::launch_grass_reset(state, d, k, static_cast<hipStream_t>(stream)),
+                    "sn_grassmann_reset launch");
+}
+
+int32_t sn_grassmann_accumulate(const void *basis, int64_t d, int64_t k, int32_t dt, const void *G,
+                                int64_t N, int64_t ldg, void *Cg, int64_t ldc, int32_t with_su,
+                                void *state, void *workspace, size_t workspace_bytes,
+                                sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if ((st = check_state(state, d, k))) return st;
+  if (N < 0 || N >= kMaxDim) return fail(SN_ERR_SHAPE, "N = %lld out of range", (long long)N);
+  if (ldg < d || ldg >= kMaxDim) return fail(SN_ERR_SHAPE, "ldg must be >= d");
+  if (Cg && (ldc < k || ldc >= kMaxDim)) return fail(SN_ERR_SHAPE, "ldc must be >= k");
+  if (N == 0) return ok();
+  if (!G) return fail(SN_ERR_NULL, "G is NULL");
+  if (!elem_aligned(G, dt) || (Cg && !elem_aligned(Cg, dt)))
+    return fail(SN_ERR_ALIGN, "G or Cg not aligned to its element size");
+  const size_t need = sn_grassmann_workspace_bytes(d, k, dt, N);
+  if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
+  const size_t es = elem_size(dt);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  const Span g = span(G, N, d, ldg, es), c = span(Cg, N, k, ldc, es);
+  const Span b = bytes_span(basis, L.total), sb = bytes_span(state, sn::grass_state_bytes(d, k));
+  const Span w = bytes_span(workspace, need);
+  if (overlap(c, g) || overlap(c, b) || overlap(c, sb) || overlap(c, w))
+    return fail(SN_ERR_ALIAS, "Cg overlaps an input, the state or the workspace");
+  if (overlap(sb, g) || overlap(sb, b) || overlap(sb, w))
+    return fail(SN_ERR_ALIAS, "state overlaps G, the basis or the workspace");
+  if (overlap(w, g) || overlap(w, b))
+    return fail(SN_ERR_ALIAS, "workspace overlaps G or the basis");
+  return hip_status(sn::launch_grass_accumulate(L, basis, G, N, ldg, Cg, ldc, with_su != 0, state,
+                                                workspace, static_cast<hipStream_t>(stream)),
+                    "sn_grassmann_accumulate launch");
+}
+
+int32_t sn_grassmann_step(const void *basis, int64_t d, int64_t k, int32_t dt, const void *state,
+                          double eta, void *U_new, int64_t ldu, int32_t out_dt, void *workspace,
+                          size_t workspace_bytes, int32_t *err_flag, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if ((st = check_state(state, d, k))) return st;
+  if (!dtype_ok(out_dt)) return fail(SN_ERR_DTYPE, "unknown out_dt %d", out_dt);
+  if (!(eta >= 0.0) || eta > 1e300) return fail(SN_ERR_SHAPE, "eta must be finite and >= 0");
+  if (!U_new) return fail(SN_ERR_NULL, "U_new is NULL");
+  if (ldu < k || ldu >= kMaxDim) return fail(SN_ERR_SHAPE, "ldu must be >= k");
+  if (!elem_aligned(U_new, out_dt)) return fail(SN_ERR_ALIGN, "U_new not aligned");
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3))
+    return fail(SN_ERR_ALIGN, "err_flag not 4-byte aligned");
+  const size_t need = sn_grassmann_workspace_bytes(d, k, dt, 0);
+  if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  const Span u = span(U_new, d, k, ldu, elem_size(out_dt));
+  const Span b = bytes_span(basis, L.total), sb = bytes_span(state, sn::grass_state_bytes(d, k));
+  const Span w = bytes_span(workspace, need);
+  if (overlap(u, b) || overlap(u, sb) || overlap(u, w))
+    return fail(SN_ERR_ALIAS, "U_new overlaps the basis, the state or the workspace");
+  if (overlap(w, b) || overlap(w, sb))
+    return fail(SN_ERR_ALIAS, "workspace overlaps the basis or the state");
+  return hip_status(sn::launch_grass_step(L, basis, state, eta, U_new, ldu, out_dt, workspace,
+                                          err_flag, static_cast<hipStream_t>(stream)),
+                    "sn_grassmann_step launch");
 }
 
 const char *sn_status_string(int32_t status) {

@@ -165,7 +165,10 @@ __device__ __forceinline__ void wait_stages(int later) {
 // (C = X U - (P U)[pos] - (T_fixed U)[tok], the subtraction done on the k
 // coefficients of each token); fp32 rows of a projected table (padded to
 // 16 ceil(k/16) columns, zero past k).
-enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2 };
+// The subspace-update epilogue (kEpiGrass) writes the fp32 coefficient rows
+// (padded like kEpiF32) and each row's sum of squares (fp64) for the
+// off-subspace loss, plus the bf16 coefficients when an output is given.
+enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2, kEpiGrass = 3 };
 
 template <int KT, bool HE, bool HP, bool PM, int EPI>
 __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__restrict__ kfrag,
@@ -173,7 +176,7 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
                                                              const bf16_t *__restrict__ X,
                                                              int64_t ldx, Tiling tm, IdArgs ids,
                                                              ProjArgs pa, void *__restrict__ Cout,
-                                                             int64_t ldc, int cvec) {
+                                                             int64_t ldc, int cvec, GrassOut go) {
   static_assert(EPI == kEpiBf16 || (!HE && !HP && !PM), "projected epilogues have no tables");
   using G = CGeo<KT, HE, HP, PM>;
   constexpr int NB = G::nb;
@@ -267,6 +270,7 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
   f32x4 acc[KT];
 #pragma unroll
   for (int t = 0; t < KT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  double sq = 0.0;  // kEpiGrass: sum of squares of the lane's elements of its row
 
   for (int s = 0; s < nst; ++s) {
     lds_barrier();  // stage s is in buffer s % NB
@@ -275,6 +279,18 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
     for (int j = 0; j < kStageCols / 32; ++j) {
       const int pc = 4 * j + g;
       const u32x4 bx = b[G::x_off + slot(xrow, pc)];
+      if constexpr (EPI == kEpiGrass) {
+        // squares of bf16 values are exact in fp32; 8 of them summed in fp32,
+        // then accumulated in fp64
+        float s8 = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float lo = bf_lo(bx[w]), hi = bf_hi(bx[w]);
+          s8 = fmaf(lo, lo, s8);
+          s8 = fmaf(hi, hi, s8);
+        }
+        sq += static_cast<double>(s8);
+      }
       u32x4 be, bpv;
       if (HE) be = neg8(b[G::e_off + slot(xrow, pc)]);
       if (HP) bpv = neg8(b[G::p_off + slot(prow, pc)]);
@@ -289,11 +305,22 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
   }
 
   // epilogue: lane (g, n) holds C[token, 16 t + 4 g .. +3]
+  if constexpr (EPI == kEpiGrass) {  // the row's four lane partials, fixed order
+    sq += __shfl_xor(sq, 16, 64);
+    sq += __shfl_xor(sq, 32, 64);
+  }
   int64_t T = T0 + wave;
   if (T >= ntiles) return;  // a tile past the end computed a duplicate
   const int64_t i = 16 * T + n;
   const int64_t tok = tm.bp == 1 ? i : tile_token(tm, T, n);
   if (tm.bp == 1 && i >= tm.N) return;
+  if constexpr (EPI == kEpiGrass) {
+#pragma unroll
+    for (int t = 0; t < KT; ++t)
+      *reinterpret_cast<f32x4 *>(go.c32 + tok * go.kp + 16 * t + 4 * g) = acc[t];
+    if (g == 0) go.gsq[tok] = sq;
+    if (!Cout) return;
+  }
   if (EPI == kEpiProjected) {
     // C = X U - (P U)[pos] - (T_fixed U)[tok], in the paper's order
     if (pa.pu) {
@@ -514,11 +541,11 @@ Tiling pick_tiling(int64_t N, const IdArgs &ids) {
 template <int KT, bool HE, bool HP, bool PM, int EPI = kEpiBf16>
 void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx, const Tiling &tm,
               const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s,
-              const ProjArgs &pa = ProjArgs{}) {
+              const ProjArgs &pa = ProjArgs{}, const GrassOut &go = GrassOut{}) {
   const int64_t ntiles = (tm.N + 15) / 16;
   dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
   compress_kernel<KT, HE, HP, PM, EPI><<<grid, kThreadsC, 0, s>>>(
-      kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec);
+      kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec, go);
 }
 
 // X U with no gathered rows, on the staged kernel (d a multiple of kStageCols)
@@ -615,6 +642,30 @@ hipError_t launch_compress_projected_mfma(const PackLayout &L, const void *packe
                                           int64_t N, int64_t ldx, const ProjArgs &pa, void *C,
                                           int64_t ldc, hipStream_t s) {
   return launch_plain<kEpiProjected>(L, packed, X, N, ldx, pa, C, ldc, s);
+}
+
+hipError_t launch_grass_compress_mfma(const PackLayout &L, const void *packed, const void *G,
+                                      int64_t N, int64_t ldg, const GrassOut &go, void *Cwire,
+                                      int64_t ldc, hipStream_t s) {
+  if (!L.mfma || L.d % kStageCols != 0) return hipErrorNotSupported;
+  const bf16_t *kf =
+      reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_kfrag);
+  const int cvec = Cwire && ((reinterpret_cast<uintptr_t>(Cwire) & 7) == 0) && (ldc % 4 == 0);
+  const Tiling tm{N, 1, 1};
+  const IdArgs none{};
+  const ProjArgs pa{};
+  switch (L.kt) {
+    case 1: launch_c<1, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 2: launch_c<2, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 3: launch_c<3, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 4: launch_c<4, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 5: launch_c<5, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 6: launch_c<6, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 7: launch_c<7, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 8: launch_c<8, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace sn

@@ -36,6 +36,8 @@ PackLayout pack_layout(int64_t d, int64_t k, int dt) {
       off = align256(off + static_cast<size_t>(d) * 32 * L.ks2 * 2);
     }
   }
+  L.off_gram = off;
+  off = align256(off + static_cast<size_t>(k) * k * 8);
   L.total = off;
   return L;
 }
@@ -102,6 +104,24 @@ __global__ __launch_bounds__(256) void pack_uu_kernel(const bf16_t *__restrict__
   out[idx] = j < 2 * k ? U[r * ldu + (j < k ? j : j - k)] : bf16_t(0);
 }
 
+// U^T U - I from the float32 section (exact copies of the stored U): one
+// workgroup per entry (a, b), float64 products summed in a fixed order.
+__global__ __launch_bounds__(256) void pack_gram_kernel(const float *__restrict__ U32, int64_t d,
+                                                        int64_t k, double *__restrict__ out) {
+  __shared__ double red[256];
+  const int64_t a = blockIdx.x / k, b = blockIdx.x - (blockIdx.x / k) * k;
+  double acc = 0.0;
+  for (int64_t r = threadIdx.x; r < d; r += 256)
+    acc += static_cast<double>(U32[r * k + a]) * static_cast<double>(U32[r * k + b]);
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (static_cast<int>(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[blockIdx.x] = red[0] - (a == b ? 1.0 : 0.0);
+}
+
 hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *packed,
                        hipStream_t s) {
   char *base = static_cast<char *>(packed);
@@ -127,6 +147,9 @@ hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *pa
           Ub, L.d, L.k, ldu, L.ks2, reinterpret_cast<bf16_t *>(base + L.off_uu));
     }
   }
+  pack_gram_kernel<<<dim3(static_cast<unsigned>(L.k * L.k)), 256, 0, s>>>(
+      reinterpret_cast<const float *>(base + L.off_f32), L.d, L.k,
+      reinterpret_cast<double *>(base + L.off_gram));
   return hipGetLastError();
 }
 

@@ -31,6 +31,8 @@ inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 //  uu    (same condition and k <= 64) [U | U] as bf16, d x 32 ceil(2k/32),
 //        columns past 2k zero: the coefficients of the weight projection's
 //        second contraction written as a decompress.
+//  gram  (every basis) U^T U - I as float64, k x k: the stored basis's
+//        departure from orthonormality, used by the off-subspace loss.
 struct PackLayout {
   int64_t d = 0, k = 0;
   int dt = 0;
@@ -38,7 +40,7 @@ struct PackLayout {
   int kt = 0;   // ceil(k/16)
   int ks = 0;   // ceil(k/32)
   int ks2 = 0;  // ceil(2k/32) when the uu section exists, else 0
-  size_t off_f32 = 0, off_kfrag = 0, off_rfrag = 0, off_uu = 0, total = 0;
+  size_t off_f32 = 0, off_kfrag = 0, off_rfrag = 0, off_uu = 0, off_gram = 0, total = 0;
 };
 
 PackLayout pack_layout(int64_t d, int64_t k, int dt);
@@ -118,6 +120,37 @@ hipError_t launch_compress_projected_generic(const PackLayout &L, const void *pa
                                              hipStream_t s);
 
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m);
+
+// ---- subspace update (Sec. 4.5) ---------------------------------------------
+// Outputs of the compress epilogue that feeds the subspace update: fp32
+// coefficient rows (row stride kp = 16 ceil(k/16), zero past k) and each
+// row's sum of squares.
+struct GrassOut {
+  float *c32 = nullptr;
+  int64_t kp = 0;
+  double *gsq = nullptr;
+};
+hipError_t launch_grass_compress_mfma(const PackLayout &L, const void *packed, const void *G,
+                                      int64_t N, int64_t ldg, const GrassOut &go, void *Cwire,
+                                      int64_t ldc, hipStream_t s);
+// Tp[split][i][j] = sum over the split's token rows n of F[n, j] G[n, i]
+// (F in the kfrag layout with ktb column tiles and npad rows, zero past N).
+hipError_t launch_grass_tokens_mfma(const void *frag, int ktb, int64_t npad, const void *G,
+                                    int64_t N, int64_t ldg, int64_t d, int64_t rows, int ds,
+                                    int64_t m_pad, float *Tp, hipStream_t s);
+
+constexpr size_t kGrassStateHead = 256;  // bytes before Y in the accumulator state
+constexpr int kGrassMaxK = 128;          // largest k of the subspace update
+size_t grass_state_bytes(int64_t d, int64_t k);
+size_t grass_workspace_bytes(const PackLayout &L, int64_t N);
+bool grass_mfma_ok(const PackLayout &L, const void *G, int64_t ldg);
+hipError_t launch_grass_reset(void *state, int64_t d, int64_t k, hipStream_t s);
+hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, const void *G,
+                                   int64_t N, int64_t ldg, void *Cwire, int64_t ldc, bool with_su,
+                                   void *state, void *ws, hipStream_t s);
+hipError_t launch_grass_step(const PackLayout &L, const void *packed, const void *state,
+                             double eta, void *Unew, int64_t ldu, int out_dt, void *ws,
+                             int32_t *err_flag, hipStream_t s);
 bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw);
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *W, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s);

@@ -99,10 +99,14 @@ template <int CW> struct P1Vec;
 template <> struct P1Vec<8> { typedef u32x4 T; };
 template <> struct P1Vec<4> { typedef u32x2 T; };
 
-template <int KT>
+// CLAMP: rows at or past nrows read row nrows - 1 instead (the caller's
+// operand is zero there), for a reduction length that is not a multiple of
+// the split size (the subspace update's contraction over tokens).
+template <int KT, bool CLAMP = false>
 __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
     const bf16_t *__restrict__ kfrag, int64_t d, const bf16_t *__restrict__ W, int64_t m,
-    int64_t ldw, int64_t rows_per_split, int64_t m_pad, float *__restrict__ Tp) {
+    int64_t ldw, int64_t rows_per_split, int64_t m_pad, float *__restrict__ Tp,
+    int64_t nrows = 0) {
   constexpr int CW = p1_cw<KT>();
   constexpr int W32 = CW / 2;  // 32-bit words per lane and row
   typedef typename P1Vec<CW>::T vec;
@@ -135,8 +139,11 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
   // rows 32 s + 8 g + e of the lane's CW columns, and the step's U fragments
   auto load = [&](int s, vec (&v)[8], u32x4 (&a)[KT]) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      v[e] = *reinterpret_cast<const vec *>(wcol + (32 * static_cast<int64_t>(s) + 8 * g + e) * ldw);
+    for (int e = 0; e < 8; ++e) {
+      int64_t row = 32 * static_cast<int64_t>(s) + 8 * g + e;
+      if constexpr (CLAMP) row = row < nrows ? row : nrows - 1;
+      v[e] = *reinterpret_cast<const vec *>(wcol + row * ldw);
+    }
 #pragma unroll
     for (int t = 0; t < KT; ++t) a[t] = ld16(ufrag + (static_cast<int64_t>(s) * KT + t) * 512);
   };
@@ -404,6 +411,37 @@ int64_t pass1_slots(int kt) {
 }
 
 }  // namespace
+
+// Subspace update, contraction over tokens: Tp[split][i][j] = sum over the
+// split's rows n of F[n, j] G[n, i], F the (npad x 16 ktb) operand in the kfrag
+// layout (zero past N), G the N x d gradient; the pass-1 kernel with the
+// roles d -> tokens, W -> G, U -> F.
+template <int KT>
+void launch_p1_tokens(const bf16_t *frag, int64_t npad, const bf16_t *G, int64_t N, int64_t ldg,
+                      int64_t d, int64_t rows, int ds, int64_t m_pad, float *Tp, hipStream_t s) {
+  dim3 grid(static_cast<unsigned>(ceil_div(d, 16 * p1_cw<KT>())), static_cast<unsigned>(ds));
+  project_pass1_kernel<KT, true><<<grid, kBlock, 0, s>>>(frag, npad, G, d, ldg, rows, m_pad, Tp,
+                                                          N);
+}
+
+hipError_t launch_grass_tokens_mfma(const void *frag, int ktb, int64_t npad, const void *G,
+                                    int64_t N, int64_t ldg, int64_t d, int64_t rows, int ds,
+                                    int64_t m_pad, float *Tp, hipStream_t s) {
+  const bf16_t *f = static_cast<const bf16_t *>(frag);
+  const bf16_t *g = static_cast<const bf16_t *>(G);
+  switch (ktb) {
+    case 1: launch_p1_tokens<1>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 2: launch_p1_tokens<2>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 3: launch_p1_tokens<3>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 4: launch_p1_tokens<4>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 5: launch_p1_tokens<5>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 6: launch_p1_tokens<6>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 7: launch_p1_tokens<7>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    case 8: launch_p1_tokens<8>(f, npad, g, N, ldg, d, rows, ds, m_pad, Tp, s); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
 
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m) {
   const int kt = static_cast<int>(ceil_div(k, 16)), ks = static_cast<int>(ceil_div(k, 32));

@@ -161,3 +161,51 @@ def test_projected_tables_validation():
     assert comp(C=out) == 5                       # C overlaps the tables
     assert comp(C=FAKE + (3 << 20)) == 5          # C overlaps X
     assert comp(N=0, X=None, C=None) == 0
+
+
+def test_grassmann_sizes_and_validation():
+    L = sn.lib()
+    # state: 256-byte head, then Y (d x k float64)
+    assert L.sn_grassmann_state_bytes(256, 8) == 256 + 256 * 8 * 8
+    assert L.sn_grassmann_state_bytes(256, 129) == 0            # k > 128
+    assert L.sn_grassmann_state_bytes(8, 9) == 0
+    ws = L.sn_grassmann_workspace_bytes(256, 8, 1, 512)
+    assert ws > 0 and ws >= L.sn_grassmann_workspace_bytes(256, 8, 1, 0) > 0
+    assert L.sn_grassmann_workspace_bytes(256, 8, 7, 512) == 0
+    state, w = FAKE + (16 << 20), FAKE + (24 << 20)
+    G, C = FAKE + (1 << 20), FAKE + (8 << 20)
+
+    def acc(**over):
+        a = dict(basis=FAKE, d=256, k=8, dt=1, G=G, N=512, ldg=256, C=C, ldc=8, su=1,
+                 state=state, ws=w, nbytes=ws)
+        a.update(over)
+        return L.sn_grassmann_accumulate(a["basis"], a["d"], a["k"], a["dt"], a["G"], a["N"],
+                                         a["ldg"], a["C"], a["ldc"], a["su"], a["state"],
+                                         a["ws"], a["nbytes"], None)
+    assert acc(basis=None) == 1
+    assert acc(state=None) == 1 and acc(state=state + 8) == 4
+    assert acc(k=129, d=512, ldg=512, ldc=129) == 8                # k above the update's limit
+    assert acc(ldg=100) == 2 and acc(ldc=7) == 2
+    assert acc(G=None) == 1 and acc(G=G + 1) == 4
+    assert acc(ws=None) == 1 and acc(ws=w + 16) == 4 and acc(nbytes=ws - 1) == 9
+    assert acc(C=G) == 5                                           # Cg overlaps G
+    assert acc(state=G) == 5                                       # state overlaps G
+    assert acc(ws=FAKE) == 5                                       # workspace overlaps the basis
+    assert acc(N=0, G=None) == 0
+
+    sw = L.sn_grassmann_workspace_bytes(256, 8, 1, 0)
+
+    def step(**over):
+        a = dict(basis=FAKE, state=state, eta=0.1, U=C, ldu=8, odt=0, ws=w, nbytes=sw, err=None)
+        a.update(over)
+        return L.sn_grassmann_step(a["basis"], 256, 8, 1, a["state"], a["eta"], a["U"], a["ldu"],
+                                   a["odt"], a["ws"], a["nbytes"], a["err"], None)
+    assert step(U=None) == 1 and step(state=None) == 1
+    assert step(eta=-1.0) == 2 and step(eta=float("nan")) == 2 and step(eta=float("inf")) == 2
+    assert step(ldu=4) == 2 and step(odt=5) == 3
+    assert step(nbytes=sw - 1) == 9
+    assert step(U=state) == 5 and step(U=w) == 5 and step(U=FAKE) == 5
+    assert step(err=C + (1 << 20) + 2) == 4
+    assert L.sn_grassmann_reset(None, 256, 8, None) == 1
+    assert L.sn_grassmann_reset(state + 64, 256, 8, None) == 4
+    assert L.sn_grassmann_reset(state, 256, 300, None) == 2
