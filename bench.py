@@ -56,6 +56,12 @@ OP_KERNELS = {
 }
 
 
+# kernels that only the subspace update launches
+GRASS_KERNELS = ["loss_kernel", "frag_kernel", "finish_kernel", "gram_partial_kernel", "gram_reduce_kernel",
+                 "update_kernel", "chol_kernel", "tri_apply_kernel", "reset_kernel",
+                 "compress_kernel<3, false, false, false, 3>"]
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -272,8 +278,15 @@ def trace_summary(trace_dir: str, bench_log: str):
              ("compress_projected+decompress loop, timed", e + pair + 6, e2),
              ("table build", e2, tb_end),
              ("compress_projected alone", tb_end, tb_end + K)]
-    if tb_end + K < len(rows):
-        cuts.append(("other configs (1, 4, 3-layer sweep; warm-up included)", tb_end + K, len(rows)))
+    at = tb_end + K
+    grass = [i for i in range(at, len(rows)) if any(
+        g in names[i] for g in GRASS_KERNELS)]
+    if grass:
+        cuts.append(("subspace update (accumulate, monitor, step; warm-up included)", at,
+                     grass[-1] + 1))
+        at = grass[-1] + 1
+    if at < len(rows):
+        cuts.append(("other configs (1, 4, 3-layer sweep; warm-up included)", at, len(rows)))
     out = os.path.join(ROOT, "profiles", "codec_step_d4096_k40_kernel_stats.md")
     with open(out, "w") as f:
         f.write("# Kernel durations: codec step at d=4096, k=40, N=32768 (bf16)\n\n")
@@ -458,6 +471,63 @@ def other_configs(sn, torch, steps: int) -> dict:
     del src, dst
     torch.cuda.empty_cache()
     return res
+
+
+def grassmann_times(sn, torch, basis, Gs, Cgs, d: int, k: int, N: int, steps: int,
+                    op_ms: dict) -> dict:
+    """The subspace update of Sec. 4.5 at the step's shape: the per-iteration
+    accumulation (gradient coefficients for the wire, the off-subspace loss and
+    Y += G^T (G U)), the loss monitor alone, and the step with its QR
+    retraction.  Mean ms per call over the same rotating gradient buffers."""
+    R = len(Gs)
+    state = sn.sn_grassmann_state(basis)
+    wsb = sn.sn_grassmann_workspace_bytes(d, k, basis.dt, N)
+    wsg = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        for i in range(2):
+            fn(i)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(reps):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    acc_ms = timed(lambda i: sn.sn_grassmann_accumulate(basis, Gs[i % R], state, out=Cgs[i % R],
+                                                        workspace=wsg), steps)
+    mon_ms = timed(lambda i: sn.sn_grassmann_accumulate(basis, Gs[i % R], state, with_su=False,
+                                                        out=Cgs[i % R], workspace=wsg), steps)
+    Un = torch.empty(d, k, dtype=torch.bfloat16, device="cuda")
+    step_ms = timed(lambda i: sn.sn_grassmann_step(basis, state, 1e-3, out=Un, workspace=wsg),
+                    max(3, steps // 4))
+    del wsg
+    es = 2
+    # what one iteration must move: G once, the wire coefficients, Y read and written, U
+    acc_bytes = N * d * es + N * k * es + 2 * d * k * 8 + d * k * es
+    mon_bytes = N * d * es + N * k * es + d * k * es
+
+    def rate(nbytes, ms):
+        return nbytes / (ms * 1e-3) / 1e9
+
+    return {
+        "accumulate_ms": round(acc_ms, 5),
+        "accumulate_bytes": acc_bytes,
+        "accumulate_GBps": round(rate(acc_bytes, acc_ms), 1),
+        "accumulate_frac_hbm": round(rate(acc_bytes, acc_ms) / HBM_PEAK_GBS, 4),
+        "accumulate_reads_of_G": 2,
+        "monitor_ms": round(mon_ms, 5),
+        "monitor_GBps": round(rate(mon_bytes, mon_ms), 1),
+        "grad_compress_ms": round(op_ms["grad_compress"], 5),
+        "step_ms": round(step_ms, 5),
+        "step_per_iteration_at_500_ms": round(step_ms / 500, 6),
+        "su_flops_per_iteration": 4 * N * d * k,
+        "paper_s_accumulation_flops_per_iteration": 2 * N * d * d,
+        "paper_s_accumulation_ms_at_bf16_peak": round(2 * N * d * d / 2.5e15 * 1e3, 4),
+    }
 
 
 def load_traffic():
@@ -731,6 +801,8 @@ def main():
                      "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": dom_traffic,
                      "algorithmic_bytes": op_bytes[dom]},
     }
+    out["grassmann"] = grassmann_times(sn, torch, basis, Gs, Cgs, d, k, N, K, op_ms)
+    print("[bench] subspace update timed", file=sys.stderr, flush=True)
     if not args.no_other_configs:
         del Xs, Gs, Cs, Cgs, Cps, Xrs, Grs, weights
         torch.cuda.empty_cache()

@@ -235,7 +235,9 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
       const int st = phys(si);
       const int64_t col = static_cast<int64_t>(st) * kStageCols;
       if (role == 0) {
-        dma_rows<kTokens, true>(rx, col, b + G::x_off, q, m);
+        // non-temporal unless the rows are read again (the subspace update's
+        // second pass reads G in reverse order, from the Infinity Cache)
+        dma_rows<kTokens, EPI != kEpiGrass>(rx, col, b + G::x_off, q, m);
       } else if (role == 1) {
         if (HE) dma_rows(re, col, b + G::e_off, q, m);
         if (HP) dma_rows(rp, col, b + G::p_off, q, m);

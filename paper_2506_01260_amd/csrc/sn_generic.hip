@@ -37,7 +37,7 @@ PackLayout pack_layout(int64_t d, int64_t k, int dt) {
     }
   }
   L.off_gram = off;
-  off = align256(off + static_cast<size_t>(k) * k * 8);
+  off = align256(off + static_cast<size_t>(16 * L.kt) * (16 * L.kt) * 8);
   L.total = off;
   return L;
 }
@@ -104,12 +104,18 @@ __global__ __launch_bounds__(256) void pack_uu_kernel(const bf16_t *__restrict__
   out[idx] = j < 2 * k ? U[r * ldu + (j < k ? j : j - k)] : bf16_t(0);
 }
 
-// U^T U - I from the float32 section (exact copies of the stored U): one
-// workgroup per entry (a, b), float64 products summed in a fixed order.
+// U^T U - I from the float32 section (exact copies of the stored U), as a
+// kp x kp matrix (kp = 16 ceil(k/16), zero outside k x k): one workgroup per
+// entry (a, b), float64 products summed in a fixed order.
 __global__ __launch_bounds__(256) void pack_gram_kernel(const float *__restrict__ U32, int64_t d,
-                                                        int64_t k, double *__restrict__ out) {
+                                                        int64_t k, int64_t kp,
+                                                        double *__restrict__ out) {
   __shared__ double red[256];
-  const int64_t a = blockIdx.x / k, b = blockIdx.x - (blockIdx.x / k) * k;
+  const int64_t a = blockIdx.x / kp, b = blockIdx.x - (blockIdx.x / kp) * kp;
+  if (a >= k || b >= k) {
+    if (threadIdx.x == 0) out[blockIdx.x] = 0.0;
+    return;
+  }
   double acc = 0.0;
   for (int64_t r = threadIdx.x; r < d; r += 256)
     acc += static_cast<double>(U32[r * k + a]) * static_cast<double>(U32[r * k + b]);
@@ -147,8 +153,9 @@ hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *pa
           Ub, L.d, L.k, ldu, L.ks2, reinterpret_cast<bf16_t *>(base + L.off_uu));
     }
   }
-  pack_gram_kernel<<<dim3(static_cast<unsigned>(L.k * L.k)), 256, 0, s>>>(
-      reinterpret_cast<const float *>(base + L.off_f32), L.d, L.k,
+  const int64_t kp = 16 * L.kt;
+  pack_gram_kernel<<<dim3(static_cast<unsigned>(kp * kp)), 256, 0, s>>>(
+      reinterpret_cast<const float *>(base + L.off_f32), L.d, L.k, kp,
       reinterpret_cast<double *>(base + L.off_gram));
   return hipGetLastError();
 }

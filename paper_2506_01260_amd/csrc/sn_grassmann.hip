@@ -17,8 +17,9 @@
 // MFMA path (bf16, d a multiple of 64, k <= 128), per accumulate:
 //   1. the staged compress kernel with the subspace-update epilogue: C in
 //      fp32 (and bf16 for the wire when asked) and each row's |g|^2;
-//   2. rows_kernel: C split into bf16 hi + lo in the MFMA operand layout of a
-//      contraction over tokens, and the rows' loss terms summed per 256 rows;
+//   2. loss_kernel: the rows' loss terms summed per 256 rows; frag_kernel: C
+//      split into bf16 hi + lo in the MFMA operand layout of a contraction
+//      over tokens;
 //   3. the weight projection's pass-1 kernel with tokens as the contraction:
 //      Tp[split][i][j] = sum over the split's rows of C_hi/lo[n, j] G[n, i];
 //   4. finish_kernel: Y += the splits and halves in a fixed order (float64),
@@ -47,14 +48,14 @@ struct AccPlan {
   int64_t rows = 0;    // tokens per split, a multiple of 128
   int64_t npad = 0;    // ds * rows >= N
   int64_t m_pad = 0;   // d rounded up to 128
-  int64_t nlblk = 0;   // loss blocks of 256 rows
+  int64_t nlblk = 0;   // loss blocks (64 rows on the MFMA path, 256 on the generic)
   size_t off_c = 0, off_gsq = 0, off_frag = 0, off_part = 0, off_tp = 0, total = 0;
 };
 
 AccPlan acc_plan(const PackLayout &L, int64_t N, bool mfma) {
   AccPlan P;
   P.mfma = mfma;
-  P.nlblk = ceil_div(N, 256);
+  P.nlblk = mfma ? ceil_div(N, 64) : ceil_div(N, 256);
   size_t off = 0;
   if (mfma) {
     P.kt = L.kt;
@@ -100,8 +101,8 @@ struct StepPlan {
 
 StepPlan step_plan(int64_t d, int64_t k) {
   StepPlan P;
-  P.nch = ceil_div(d, 64);
-  if (P.nch > 64) P.nch = 64;
+  P.nch = ceil_div(d, 32);
+  if (P.nch > 256) P.nch = 256;
   P.rpc = ceil_div(d, P.nch);
   P.nch = ceil_div(d, P.rpc);
   const size_t dk = static_cast<size_t>(d) * k * 8, kk = static_cast<size_t>(k) * k * 8;
@@ -165,76 +166,122 @@ __global__ __launch_bounds__(256) void reset_kernel(double *__restrict__ state, 
 // ---------------------------------------------------------------------------
 // accumulate, MFMA path
 // ---------------------------------------------------------------------------
-// Blocks [0, nfrag_blocks): one thread per (operand part, token step s,
-// column tile t, lane) writes the 8 bf16 F[32 s + 8 g + e, 16 t + n] of the
-// kfrag layout.  Column c of operand 1 of 1 is C_hi[:, c] for c < k and
-// C_lo[:, c - k] for k <= c < 2k; of 2 operands, part 0 is C_hi and part 1
-// C_lo.  Zero past the columns and past row N.
-// Blocks past them: one thread per row, loss term |g|^2 - |c|^2 + c D c^T,
-// summed per block of 256 rows.
-__global__ __launch_bounds__(256) void rows_kernel(
-    const float *__restrict__ c32, int64_t kp, const double *__restrict__ gsq,
-    const double *__restrict__ dgram, int64_t N, int64_t k, int nparts, int ktb, int64_t npad,
-    bf16_t *__restrict__ frag, int64_t nfrag_blocks, double *__restrict__ part) {
-  __shared__ double red[256];
-  if (static_cast<int64_t>(blockIdx.x) < nfrag_blocks) {
-    const int64_t slot = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    const int64_t per_part = (npad / 32) * ktb * 64;
-    if (slot >= nparts * per_part) return;
-    const int p = static_cast<int>(slot / per_part);
-    const int64_t rem = slot - p * per_part;
-    const int64_t blk = rem >> 6;
-    const int lane = static_cast<int>(rem & 63);
-    const int64_t s = blk / ktb;
-    const int64_t t = blk - s * ktb;
-    const int g = lane >> 4, n = lane & 15;
-    const int64_t c2 = 16 * t + n;
-    bool lo;
-    int64_t col;
-    if (nparts == 1) {
-      lo = c2 >= k;
-      col = lo ? c2 - k : c2;
-    } else {
-      lo = p == 1;
-      col = c2;
-    }
-    const bool cvalid = col < k;
-    uint32_t w[4];
+// One thread per (operand part, token step s, column tile t, lane) writes the
+// 8 bf16 F[32 s + 8 g + e, 16 t + n] of the kfrag layout.  Column c of
+// operand 1 of 1 is C_hi[:, c] for c < k and C_lo[:, c - k] for k <= c < 2k;
+// of 2 operands, part 0 is C_hi and part 1 C_lo.  Zero past the columns and
+// past row N.
+__global__ __launch_bounds__(256) void frag_kernel(const float *__restrict__ c32, int64_t kp,
+                                                   int64_t N, int64_t k, int nparts, int ktb,
+                                                   int64_t npad, bf16_t *__restrict__ frag) {
+  const int64_t slot = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t per_part = (npad / 32) * ktb * 64;
+  if (slot >= nparts * per_part) return;
+  const int p = static_cast<int>(slot / per_part);
+  const int64_t rem = slot - p * per_part;
+  const int64_t blk = rem >> 6;
+  const int lane = static_cast<int>(rem & 63);
+  const int64_t s = blk / ktb;
+  const int64_t t = blk - s * ktb;
+  const int g = lane >> 4, n = lane & 15;
+  const int64_t c2 = 16 * t + n;
+  bool lo;
+  int64_t col;
+  if (nparts == 1) {
+    lo = c2 >= k;
+    col = lo ? c2 - k : c2;
+  } else {
+    lo = p == 1;
+    col = c2;
+  }
+  const bool cvalid = col < k;
+  uint32_t w[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      bf16_t h[2];
+  for (int q = 0; q < 4; ++q) {
+    bf16_t h[2];
 #pragma unroll
-      for (int e2 = 0; e2 < 2; ++e2) {
-        const int64_t row = 32 * s + 8 * g + 2 * q + e2;
-        h[e2] = bf16_t(0);
-        if (cvalid && row < N) {
-          const float x = c32[row * kp + col];
-          const bf16_t hi = from_f32<bf16_t>(x);
-          h[e2] = lo ? from_f32<bf16_t>(x - to_f32(hi)) : hi;
-        }
+    for (int e2 = 0; e2 < 2; ++e2) {
+      const int64_t row = 32 * s + 8 * g + 2 * q + e2;
+      h[e2] = bf16_t(0);
+      if (cvalid && row < N) {
+        const float x = c32[row * kp + col];
+        const bf16_t hi = from_f32<bf16_t>(x);
+        h[e2] = lo ? from_f32<bf16_t>(x - to_f32(hi)) : hi;
       }
-      w[q] = static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
     }
-    *reinterpret_cast<u32x4 *>(frag + slot * 8) = u32x4{w[0], w[1], w[2], w[3]};
-    return;
+    w[q] = static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
   }
-  const int64_t lb = static_cast<int64_t>(blockIdx.x) - nfrag_blocks;
-  const int64_t row = lb * 256 + threadIdx.x;
-  double l = 0.0;
-  if (row < N) {
-    const float *c = c32 + row * kp;
-    double cc = 0.0, q = 0.0;
-    for (int64_t a = 0; a < k; ++a) {
-      const double ca = c[a];
+  *reinterpret_cast<u32x4 *>(frag + slot * 8) = u32x4{w[0], w[1], w[2], w[3]};
+}
+
+// Loss terms |g|^2 - |c|^2 + c D c^T of 64 rows per block, summed: the
+// block's coefficient rows are staged in LDS with coalesced loads (row stride
+// 16 KT + 1 words, so per-lane row reads hit distinct banks); wave w takes the
+// coefficient indices a = w, w + 4, ... of every row (lane = row), with D's row
+// a read by uniform loads (D is padded to 16 KT columns, and so are the rows:
+// the padding is zero on both sides); the four waves' sums meet in LDS in a
+// fixed order.
+template <int KT>
+__global__ __launch_bounds__(256) void loss_kernel(const float *__restrict__ c32,
+                                                   const double *__restrict__ gsq,
+                                                   const double *__restrict__ dgram, int64_t N,
+                                                   int64_t k, double *__restrict__ part) {
+  constexpr int KP = 16 * KT, LDL = KP + 1;
+  __shared__ float cs[64 * LDL];
+  __shared__ double red[256];
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 64;
+  const int64_t nr = N - r0 < 64 ? N - r0 : 64;
+  for (int64_t e = threadIdx.x; e < nr * KP; e += 256)
+    cs[(e / KP) * LDL + e % KP] = c32[r0 * KP + e];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  (void)k;  // rows and columns of D past k are zero, and so are c's
+  double cc = 0.0, q = 0.0;
+  if (lane < nr) {
+    const float *c = cs + lane * LDL;
+    double r[KP / 4];  // (D c)_a for a = w + 4 i
+#pragma unroll
+    for (int i = 0; i < KP / 4; ++i) r[i] = 0.0;
+#pragma unroll 4
+    for (int b = 0; b < KP; ++b) {
+      const double cb = c[b];
+#pragma unroll
+      for (int i = 0; i < KP / 4; ++i) r[i] += dgram[(w + 4 * i) * KP + b] * cb;
+    }
+#pragma unroll
+    for (int i = 0; i < KP / 4; ++i) {
+      const double ca = c[w + 4 * i];
       cc += ca * ca;
-      double r = 0.0;
-      for (int64_t b = 0; b < k; ++b) r += dgram[a * k + b] * static_cast<double>(c[b]);
-      q += ca * r;
+      q += ca * r[i];
     }
-    l = gsq[row] - cc + q;
   }
+  red[threadIdx.x] = q - cc;
+  __syncthreads();
+  double l = 0.0;
+  if (w == 0 && lane < nr)
+    l = gsq[r0 + lane] + (((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane]);
+  __syncthreads();
   const double tot = block_sum256(l, red);
-  if (threadIdx.x == 0) part[lb] = tot;
+  if (threadIdx.x == 0) part[blockIdx.x] = tot;
+}
+
+hipError_t launch_loss(int kt, const float *c32, const double *gsq, const double *dgram,
+                       int64_t N, int64_t k, double *part, int64_t nlblk, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(ceil_div(N, 64)));
+  (void)nlblk;
+  switch (kt) {
+    case 1: loss_kernel<1><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 2: loss_kernel<2><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 3: loss_kernel<3><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 4: loss_kernel<4><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 5: loss_kernel<5><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 6: loss_kernel<6><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 7: loss_kernel<7><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 8: loss_kernel<8><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -312,9 +359,13 @@ __global__ __launch_bounds__(256) void finish_kernel(const float *__restrict__ t
     }
     state_y(state)[idx] += acc;
   }
-  if (idx == 0) {
-    double sum = 0.0;
-    for (int64_t b = 0; b < nlblk; ++b) sum += part[b];
+  if (blockIdx.x != 0) return;
+  // block 0: the loss partials, each thread a strided subset in order, then a tree
+  __shared__ double red[256];
+  double v = 0.0;
+  for (int64_t b = threadIdx.x; b < nlblk; b += 256) v += part[b];
+  const double sum = block_sum256(v, red);
+  if (threadIdx.x == 0) {
     state[0] += sum;
     state[1] += 1.0;
     state[2] = state[0] / state[1];
@@ -325,20 +376,48 @@ __global__ __launch_bounds__(256) void finish_kernel(const float *__restrict__ t
 // ---------------------------------------------------------------------------
 // step
 // ---------------------------------------------------------------------------
-// partial[c][a * k + b] = sum over the rows r of chunk c of A[r, a] B[r, b]
+// partial[c][a * k + b] = sum over the rows r of chunk c of A[r, a] B[r, b];
+// the chunk's rows (at most kGramRows) are staged in LDS as float64.
+constexpr int kGramRows = 32;
 template <typename TA, typename TB>
 __global__ __launch_bounds__(256) void gram_partial_kernel(const TA *__restrict__ A, int64_t lda,
                                                            const TB *__restrict__ B, int64_t ldb,
                                                            int64_t d, int64_t k, int64_t rpc,
                                                            double *__restrict__ partial) {
+  __shared__ double sa[kGramRows * kGrassMaxK], sb[kGramRows * kGrassMaxK];
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rpc;
   const int64_t r1 = r0 + rpc < d ? r0 + rpc : d;
-  for (int64_t o = threadIdx.x; o < k * k; o += 256) {
-    const int64_t a = o / k, b = o - (o / k) * k;
-    double acc = 0.0;
-    for (int64_t r = r0; r < r1; ++r)
-      acc += static_cast<double>(A[r * lda + a]) * static_cast<double>(B[r * ldb + b]);
-    partial[blockIdx.x * k * k + o] = acc;
+  const int64_t kk = k * k;
+  // outputs in groups of 16 per thread (k <= 64: one group)
+  for (int64_t og = 0; og < kk; og += 16 * 256) {
+    double acc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.0;
+    for (int64_t c0 = r0; c0 < r1; c0 += kGramRows) {
+      const int64_t nrow = r1 - c0 < kGramRows ? r1 - c0 : kGramRows;
+      __syncthreads();
+      for (int64_t e = threadIdx.x; e < nrow * k; e += 256) {
+        const int64_t rr = e / k, cc = e - (e / k) * k;
+        sa[e] = static_cast<double>(A[(c0 + rr) * lda + cc]);
+        sb[e] = static_cast<double>(B[(c0 + rr) * ldb + cc]);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int64_t o = og + threadIdx.x + 256 * i;
+        if (o < kk) {
+          const int64_t a = o / k, b = o - (o / k) * k;
+          double v = acc[i];
+          for (int64_t rr = 0; rr < nrow; ++rr) v += sa[rr * k + a] * sb[rr * k + b];
+          acc[i] = v;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t o = og + threadIdx.x + 256 * i;
+      if (o < kk) partial[blockIdx.x * kk + o] = acc[i];
+    }
   }
 }
 
@@ -348,6 +427,7 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const double *__restri
   const int64_t o = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (o >= kk) return;
   double acc = 0.0;
+#pragma unroll 8
   for (int64_t c = 0; c < nch; ++c) acc += partial[c * kk + o];
   out[o] = acc;
 }
@@ -373,17 +453,24 @@ __global__ __launch_bounds__(256) void update_kernel(const float *__restrict__ U
   A[idx] = static_cast<double>(U32[idx]) + sc * acc;
 }
 
-// Cholesky factor R (upper, positive diagonal) of the k x k Gram matrix:
-// gram = R^T R.  One workgroup; a non-positive pivot sets *status.
-__global__ __launch_bounds__(256) void chol_kernel(const double *__restrict__ gram, int64_t k,
-                                                   double *__restrict__ R, int *__restrict__ status) {
+// Cholesky factor R (upper, positive diagonal) of the k x k Gram matrix,
+// gram = R^T R, and its inverse X = R^{-1} (upper), written to Rinv: one
+// workgroup, everything in LDS.  A non-positive, NaN or overflowing pivot
+// sets *status.
+__global__ __launch_bounds__(256) void chol_kernel(const double *__restrict__ gram, int64_t k64,
+                                                   double *__restrict__ Rinv,
+                                                   int *__restrict__ status) {
   __shared__ double A[kGrassMaxK][kGrassMaxK + 1];
+  __shared__ double xd[kGrassMaxK];
   __shared__ int bad;
-  for (int64_t o = threadIdx.x; o < k * k; o += 256) A[o / k][o % k] = gram[o];
-  if (threadIdx.x == 0) bad = 0;
+  const int k = static_cast<int>(k64);
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;  // 16 x 16 thread grid
+  for (int i = ty; i < k; i += 16)
+    for (int l = tx; l < k; l += 16) A[i][l] = gram[i * k + l];
+  if (tid == 0) bad = 0;
   __syncthreads();
-  for (int64_t j = 0; j < k; ++j) {
-    if (threadIdx.x == 0) {
+  for (int j = 0; j < k; ++j) {
+    if (tid == 0) {
       double p = A[j][j];
       if (!(p > 0.0 && p <= 1.0e300)) {  // non-positive, NaN or overflowing pivot
         bad = 1;
@@ -392,55 +479,58 @@ __global__ __launch_bounds__(256) void chol_kernel(const double *__restrict__ gr
       A[j][j] = sqrt(p);
     }
     __syncthreads();
-    const double rjj = A[j][j];
-    for (int64_t l = j + 1 + threadIdx.x; l < k; l += 256) A[j][l] /= rjj;
+    const double inv = 1.0 / A[j][j];
+    for (int l = j + 1 + tid; l < k; l += 256) A[j][l] *= inv;
     __syncthreads();
-    const int64_t m = k - j - 1;
-    for (int64_t o = threadIdx.x; o < m * m; o += 256) {
-      const int64_t i = j + 1 + o / m, l = j + 1 + o % m;
-      if (l >= i) A[i][l] -= A[j][i] * A[j][l];
+    for (int i = j + 1 + ty; i < k; i += 16) {
+      const double rji = A[j][i];
+      for (int l = i + ((tx - i) % 16 + 16) % 16; l < k; l += 16) A[i][l] -= rji * A[j][l];
     }
     __syncthreads();
   }
-  for (int64_t o = threadIdx.x; o < k * k; o += 256) {
-    const int64_t i = o / k, l = o % k;
-    R[o] = l >= i ? A[i][l] : 0.0;
+  // X = R^{-1}: thread b solves R x = e_b by back substitution; x_i (i < b)
+  // is kept at A[b][i], below the diagonal (the factor lives on and above
+  // it), and x_b in xd[b]
+  for (int b = tid; b < k; b += 256) {
+    xd[b] = 1.0 / A[b][b];
+    for (int i = b - 1; i >= 0; --i) {
+      double v = -A[i][b] * xd[b];
+      for (int l = i + 1; l < b; ++l) v -= A[i][l] * A[b][l];
+      A[b][i] = v / A[i][i];
+    }
   }
-  if (threadIdx.x == 0 && bad) *status = 1;
+  __syncthreads();
+  for (int i = ty; i < k; i += 16)
+    for (int b = tx; b < k; b += 16) Rinv[i * k + b] = i < b ? A[b][i] : (i == b ? xd[b] : 0.0);
+  if (tid == 0 && bad) *status = 1;
 }
 
-// Q = A R^{-1}, one row per thread: q R = a solved by forward substitution
-// over the columns.  OUT 0: float64 to the workspace; OUT 1 / 2: the new
-// basis as float32 / bf16 (rounded once from float64), or the old basis
-// unchanged when either Cholesky factorisation failed.
+// Q = A R^{-1}, one thread per element: Q[r, b] = sum_{a <= b} A[r, a] X[a, b].
+// OUT 0: float64 to the workspace; OUT 1 / 2: the new basis as float32 / bf16
+// (rounded once from float64), or the old basis unchanged when either
+// Cholesky factorisation failed.
 template <int OUT>
-__global__ __launch_bounds__(64) void tri_apply_kernel(const double *__restrict__ A,
-                                                       const double *__restrict__ R, int64_t d,
-                                                       int64_t k, const int *__restrict__ status,
-                                                       const float *__restrict__ U32, void *out,
-                                                       int64_t ldo, int32_t *err_flag) {
-  __shared__ double q[64][kGrassMaxK + 1];
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * 64 + threadIdx.x;
-  if (r >= d) return;
-  const int t = threadIdx.x;
-  for (int64_t b = 0; b < k; ++b) {
-    double v = A[r * k + b];
-    for (int64_t a = 0; a < b; ++a) v -= q[t][a] * R[a * k + b];
-    q[t][b] = v / R[b * k + b];
-  }
+__global__ __launch_bounds__(256) void tri_apply_kernel(const double *__restrict__ A,
+                                                        const double *__restrict__ Rinv,
+                                                        int64_t d, int64_t k,
+                                                        const int *__restrict__ status,
+                                                        const float *__restrict__ U32, void *out,
+                                                        int64_t ldo, int32_t *err_flag) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= d * k) return;
+  const int64_t r = idx / k, b = idx - (idx / k) * k;
+  double v = 0.0;
+  for (int64_t a = 0; a <= b; ++a) v += A[r * k + a] * Rinv[a * k + b];
   if constexpr (OUT == 0) {
-    double *o = static_cast<double *>(out) + r * ldo;
-    for (int64_t b = 0; b < k; ++b) o[b] = q[t][b];
+    static_cast<double *>(out)[r * ldo + b] = v;
   } else {
     const bool failed = status[0] != 0 || status[1] != 0;
-    if (failed && r == 0 && err_flag) atomicOr(err_flag, 4);
-    for (int64_t b = 0; b < k; ++b) {
-      const double v = failed ? static_cast<double>(U32[r * k + b]) : q[t][b];
-      if constexpr (OUT == 1)
-        static_cast<float *>(out)[r * ldo + b] = static_cast<float>(v);
-      else
-        static_cast<bf16_t *>(out)[r * ldo + b] = bf16_from_f64(v);
-    }
+    if (failed && idx == 0 && err_flag) atomicOr(err_flag, 4);
+    if (failed) v = static_cast<double>(U32[r * k + b]);
+    if constexpr (OUT == 1)
+      static_cast<float *>(out)[r * ldo + b] = static_cast<float>(v);
+    else
+      static_cast<bf16_t *>(out)[r * ldo + b] = bf16_from_f64(v);
   }
 }
 
@@ -497,13 +587,16 @@ hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, cons
     go.gsq = reinterpret_cast<double *>(w + P.off_gsq);
     hipError_t e = launch_grass_compress_mfma(L, packed, G, N, ldg, go, Cwire, ldc, s);
     if (e != hipSuccess) return e;
+    e = launch_loss(P.kt, go.c32, go.gsq, reinterpret_cast<const double *>(base + L.off_gram),
+                    N, L.k, part, P.nlblk, s);
+    if (e != hipSuccess) return e;
     bf16_t *frag = reinterpret_cast<bf16_t *>(w + P.off_frag);
-    const int64_t nfrag = with_su ? ceil_div(P.nparts * (P.npad / 32) * P.ktb * 64, 256) : 0;
-    rows_kernel<<<dim3(static_cast<unsigned>(nfrag + P.nlblk)), 256, 0, s>>>(
-        go.c32, go.kp, go.gsq, reinterpret_cast<const double *>(base + L.off_gram), N, L.k,
-        P.nparts, P.ktb, P.npad, frag, nfrag, part);
     float *tp = reinterpret_cast<float *>(w + P.off_tp);
     if (with_su) {
+      const int64_t nfrag = ceil_div(P.nparts * (P.npad / 32) * P.ktb * 64, 256);
+      frag_kernel<<<dim3(static_cast<unsigned>(nfrag)), 256, 0, s>>>(go.c32, go.kp, N, L.k,
+                                                                     P.nparts, P.ktb, P.npad,
+                                                                     frag);
       const int64_t per_part = static_cast<int64_t>(P.npad / 32) * P.ktb * 512;
       for (int p = 0; p < P.nparts; ++p) {
         e = launch_grass_tokens_mfma(frag + p * per_part, P.ktb, P.npad, G, N, ldg, L.d, P.rows,
@@ -566,19 +659,18 @@ hipError_t launch_grass_step(const PackLayout &L, const void *packed, const void
   double *R = reinterpret_cast<double *>(w + P.off_r);
   int *status = reinterpret_cast<int *>(w + P.off_status);
   const dim3 gdk(static_cast<unsigned>(ceil_div(d * k, 256)));
-  const dim3 grows(static_cast<unsigned>(ceil_div(d, 64)));
 
   gram<float, double>(U32, k, Y, k, d, k, P, part, Z, s);                 // Z = U^T Y
   update_kernel<<<gdk, 256, 0, s>>>(U32, st, Z, eta, d, k, A, status);    // A = U - eta T
   gram<double, double>(A, k, A, k, d, k, P, part, Gm, s);                 // A^T A
   chol_kernel<<<dim3(1), 256, 0, s>>>(Gm, k, R, status);
-  tri_apply_kernel<0><<<grows, 64, 0, s>>>(A, R, d, k, status, U32, Q, k, nullptr);
+  tri_apply_kernel<0><<<gdk, 256, 0, s>>>(A, R, d, k, status, U32, Q, k, nullptr);
   gram<double, double>(Q, k, Q, k, d, k, P, part, Gm, s);                 // Q^T Q
   chol_kernel<<<dim3(1), 256, 0, s>>>(Gm, k, R, status + 1);
   if (out_dt == 0)
-    tri_apply_kernel<1><<<grows, 64, 0, s>>>(Q, R, d, k, status, U32, Unew, ldu, err_flag);
+    tri_apply_kernel<1><<<gdk, 256, 0, s>>>(Q, R, d, k, status, U32, Unew, ldu, err_flag);
   else
-    tri_apply_kernel<2><<<grows, 64, 0, s>>>(Q, R, d, k, status, U32, Unew, ldu, err_flag);
+    tri_apply_kernel<2><<<gdk, 256, 0, s>>>(Q, R, d, k, status, U32, Unew, ldu, err_flag);
   return hipGetLastError();
 }
 

@@ -31,8 +31,9 @@ inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 //  uu    (same condition and k <= 64) [U | U] as bf16, d x 32 ceil(2k/32),
 //        columns past 2k zero: the coefficients of the weight projection's
 //        second contraction written as a decompress.
-//  gram  (every basis) U^T U - I as float64, k x k: the stored basis's
-//        departure from orthonormality, used by the off-subspace loss.
+//  gram  (every basis) U^T U - I as float64, kp x kp with kp = 16 ceil(k/16)
+//        (zero outside k x k): the stored basis's departure from
+//        orthonormality, used by the off-subspace loss.
 struct PackLayout {
   int64_t d = 0, k = 0;
   int dt = 0;

@@ -102,12 +102,11 @@ template <> struct P1Vec<4> { typedef u32x2 T; };
 // CLAMP: rows at or past nrows read row nrows - 1 instead (the caller's
 // operand is zero there), for a reduction length that is not a multiple of
 // the split size (the subspace update's contraction over tokens).
-template <int KT, bool CLAMP = false>
+template <int KT, bool CLAMP = false, int CW = p1_cw<KT>()>
 __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
     const bf16_t *__restrict__ kfrag, int64_t d, const bf16_t *__restrict__ W, int64_t m,
     int64_t ldw, int64_t rows_per_split, int64_t m_pad, float *__restrict__ Tp,
     int64_t nrows = 0) {
-  constexpr int CW = p1_cw<KT>();
   constexpr int W32 = CW / 2;  // 32-bit words per lane and row
   typedef typename P1Vec<CW>::T vec;
   __shared__ f32x4 red[KT][CW][64];
@@ -115,7 +114,9 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, n = lane & 15;
   const int64_t cb = static_cast<int64_t>(blockIdx.x) * (16 * CW);
-  const int split = blockIdx.y;
+  // CLAMP (the token contraction) takes the splits last-first: the rows the
+  // preceding pass read last are the likeliest still to be cached
+  const int split = CLAMP ? static_cast<int>(gridDim.y - 1 - blockIdx.y) : blockIdx.y;
   const int64_t col = cb + CW * n;
   const bool cvalid = col < m;  // m % 8 == 0: all CW columns are valid
 
@@ -416,12 +417,18 @@ int64_t pass1_slots(int kt) {
 // split's rows n of F[n, j] G[n, i], F the (npad x 16 ktb) operand in the kfrag
 // layout (zero past N), G the N x d gradient; the pass-1 kernel with the
 // roles d -> tokens, W -> G, U -> F.
+// 16-byte row pieces (8 columns per lane) up to 5 column tiles: the
+// accumulators then live in the AGPRs
+template <int KT>
+constexpr int tok_cw() { return KT <= 5 ? 8 : 4; }
+
 template <int KT>
 void launch_p1_tokens(const bf16_t *frag, int64_t npad, const bf16_t *G, int64_t N, int64_t ldg,
                       int64_t d, int64_t rows, int ds, int64_t m_pad, float *Tp, hipStream_t s) {
-  dim3 grid(static_cast<unsigned>(ceil_div(d, 16 * p1_cw<KT>())), static_cast<unsigned>(ds));
-  project_pass1_kernel<KT, true><<<grid, kBlock, 0, s>>>(frag, npad, G, d, ldg, rows, m_pad, Tp,
-                                                          N);
+  constexpr int CW = tok_cw<KT>();
+  dim3 grid(static_cast<unsigned>(ceil_div(d, 16 * CW)), static_cast<unsigned>(ds));
+  project_pass1_kernel<KT, true, CW><<<grid, kBlock, 0, s>>>(frag, npad, G, d, ldg, rows, m_pad,
+                                                              Tp, N);
 }
 
 hipError_t launch_grass_tokens_mfma(const void *frag, int ktb, int64_t npad, const void *G,
