@@ -53,6 +53,9 @@ OP_KERNELS = {
     "grad_compress": ["compress_kernel<3, false, false, false, 0>"],
     "grad_decompress": ["decompress_cb_kernel<2, false, false, 0>"],
     "compress_projected": ["compress_kernel<3, false, false, false, 1>"],
+    # subspace update: its compress pass and its contraction over tokens
+    "grassmann_compress": ["compress_kernel<3, false, false, false, 3>"],
+    "grassmann_tokens": ["project_pass1_kernel<5, true, 8>"],
 }
 
 
@@ -279,8 +282,8 @@ def trace_summary(trace_dir: str, bench_log: str):
              ("table build", e2, tb_end),
              ("compress_projected alone", tb_end, tb_end + K)]
     at = tb_end + K
-    grass = [i for i in range(at, len(rows)) if any(
-        g in names[i] for g in GRASS_KERNELS)]
+    grass = [i for i in range(at, len(rows))
+             if names[i] in GRASS_KERNELS or names[i].split("<")[0] in GRASS_KERNELS]
     if grass:
         cuts.append(("subspace update (accumulate, monitor, step; warm-up included)", at,
                      grass[-1] + 1))
@@ -642,9 +645,11 @@ def main():
         dst = torch.empty_like(src)
         for _ in range(3):
             torch.mul(src, 1.0, out=dst)
+        gstate = sn.sn_grassmann_state(basis)
         for i in range(3):
             step(i)
             op("compress_projected", i)
+            sn.sn_grassmann_accumulate(basis, Gs[i % R], gstate, out=Cgs[i % R])
         torch.cuda.synchronize()
         print("[bench] profile pass done", file=sys.stderr, flush=True)
         return

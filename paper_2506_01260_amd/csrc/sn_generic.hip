@@ -105,27 +105,32 @@ __global__ __launch_bounds__(256) void pack_uu_kernel(const bf16_t *__restrict__
 }
 
 // U^T U - I from the float32 section (exact copies of the stored U), as a
-// kp x kp matrix (kp = 16 ceil(k/16), zero outside k x k): one workgroup per
-// entry (a, b), float64 products summed in a fixed order.
+// kp x kp matrix (kp = 16 ceil(k/16) <= 256, zero outside k x k).  One
+// workgroup per row a; thread (h, b) sums U[r, a] U[r, b] in float64 over the
+// rows r = h mod H (H = 256 / kp row phases, reads coalesced along b), and the
+// H partial sums are added in a fixed order.
 __global__ __launch_bounds__(256) void pack_gram_kernel(const float *__restrict__ U32, int64_t d,
                                                         int64_t k, int64_t kp,
                                                         double *__restrict__ out) {
   __shared__ double red[256];
-  const int64_t a = blockIdx.x / kp, b = blockIdx.x - (blockIdx.x / kp) * kp;
-  if (a >= k || b >= k) {
-    if (threadIdx.x == 0) out[blockIdx.x] = 0.0;
-    return;
-  }
+  const int64_t a = blockIdx.x;
+  const int H = static_cast<int>(256 / kp);
+  const int h = static_cast<int>(threadIdx.x / kp), b = static_cast<int>(threadIdx.x % kp);
   double acc = 0.0;
-  for (int64_t r = threadIdx.x; r < d; r += 256)
-    acc += static_cast<double>(U32[r * k + a]) * static_cast<double>(U32[r * k + b]);
+  if (a < k && h < H && b < k) {
+#pragma unroll 4
+    for (int64_t r = h; r < d; r += H)
+      acc += static_cast<double>(U32[r * k + a]) * static_cast<double>(U32[r * k + b]);
+  }
   red[threadIdx.x] = acc;
   __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if (static_cast<int>(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
+  if (threadIdx.x < kp) {
+    double v = 0.0;
+    for (int hh = 0; hh < H; ++hh) v += red[hh * kp + threadIdx.x];
+    const bool in = a < k && static_cast<int64_t>(threadIdx.x) < k;
+    out[a * kp + threadIdx.x] = in ? v - (a == static_cast<int64_t>(threadIdx.x) ? 1.0 : 0.0)
+                                   : 0.0;
   }
-  if (threadIdx.x == 0) out[blockIdx.x] = red[0] - (a == b ? 1.0 : 0.0);
 }
 
 hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *packed,
@@ -154,7 +159,7 @@ hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *pa
     }
   }
   const int64_t kp = 16 * L.kt;
-  pack_gram_kernel<<<dim3(static_cast<unsigned>(kp * kp)), 256, 0, s>>>(
+  pack_gram_kernel<<<dim3(static_cast<unsigned>(kp)), 256, 0, s>>>(
       reinterpret_cast<const float *>(base + L.off_f32), L.d, L.k, kp,
       reinterpret_cast<double *>(base + L.off_gram));
   return hipGetLastError();
