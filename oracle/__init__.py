@@ -16,7 +16,8 @@ the output dtype with round-to-nearest-even:
   projection matrices confined to S = Col(U); Appendix E's projection Pi_S)
 
 The subspace update of Section 4.5 (off-subspace loss, accumulation matrix,
-Riemannian gradient, QR retraction) is in ``grassmann``.
+Riemannian gradient, QR retraction) is in ``grassmann``; the modified AdamW
+step of Section 5 in ``adamw``.
 
 ``exact`` holds the same operations in exact rational arithmetic
 (``fractions.Fraction``) for brute-force checks on tiny inputs.
@@ -24,8 +25,8 @@ Riemannian gradient, QR retraction) is in ``grassmann``.
 from .bf16 import decode_bf16, encode_bf16, round_bf16, round_f32, round_to
 from .codec import (compress, decompress, grad_compress, grad_decompress,
                     project_weights, default_positions)
-from . import grassmann
+from . import adamw, grassmann
 
 __all__ = ["decode_bf16", "encode_bf16", "round_bf16", "round_f32", "round_to",
            "compress", "decompress", "grad_compress", "grad_decompress",
-           "project_weights", "default_positions", "grassmann"]
+           "project_weights", "default_positions", "grassmann", "adamw"]
