@@ -533,6 +533,51 @@ def grassmann_times(sn, torch, basis, Gs, Cgs, d: int, k: int, N: int, steps: in
     }
 
 
+def adamw_times(sn, torch, weights, steps: int) -> dict:
+    """The modified AdamW step of Sec. 5 (column-constant rate) and the
+    standard one on the step's weight matrices (bf16 W and G, fp32 moments),
+    mean ms per call over two rotating sets."""
+    out = {}
+    for i, Wl in enumerate(weights):
+        rows, cols = Wl[0].shape
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(7 + i)
+        sets = []
+        for j in range(2):
+            G = (torch.randn(rows, cols, device="cuda", generator=gen) * 1e-3).to(torch.bfloat16)
+            M = torch.zeros(rows, cols, device="cuda")
+            V = torch.zeros(rows, cols, device="cuda")
+            sets.append((Wl[j], G, M, V))
+        ws = torch.empty(sn.sn_adamw_workspace_bytes(rows, cols), dtype=torch.uint8,
+                         device="cuda")
+        stream = torch.cuda.current_stream()
+        res = {}
+        for name, sub in (("subspace", True), ("standard", False)):
+            def call(t):
+                W, G, M, V = sets[t % 2]
+                sn.sn_adamw_step(W, G, M, V, t + 1, lr=1e-6, weight_decay=0.0, subspace=sub,
+                                 workspace=ws)
+            for t in range(2):
+                call(t)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for t in range(steps):
+                call(2 + t)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b) / steps
+            # read G, M, V, W and write M, V, W once each (the subspace form reads M twice)
+            nbytes = rows * cols * (2 + 4 + 4 + 2 + 4 + 4 + 2)
+            res[name] = {"ms": round(ms, 5), "bytes": nbytes,
+                         "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                         "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        out[f"W{i}_{rows}x{cols}"] = res
+        del sets, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def load_traffic():
     try:
         t = json.load(open(TRAFFIC_FILE))
@@ -808,6 +853,8 @@ def main():
     }
     out["grassmann"] = grassmann_times(sn, torch, basis, Gs, Cgs, d, k, N, K, op_ms)
     print("[bench] subspace update timed", file=sys.stderr, flush=True)
+    out["adamw"] = adamw_times(sn, torch, weights, K)
+    print("[bench] AdamW timed", file=sys.stderr, flush=True)
     if not args.no_other_configs:
         del Xs, Gs, Cs, Cgs, Cps, Xrs, Grs, weights
         torch.cuda.empty_cache()

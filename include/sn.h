@@ -296,6 +296,52 @@ int32_t sn_grassmann_step(const void *basis, int64_t d, int64_t k, int32_t dt,
                           sn_stream stream);
 
 /* ------------------------------------------------------------------------ */
+/* Modified AdamW (Sec. 5).                                                   */
+/*                                                                            */
+/* W_p2's rows lie in S in the paper's layout; stored [out, in] (d x m, as    */
+/* sn_project_weights takes it) its COLUMNS lie in S.  AdamW's entrywise rate */
+/* 1 / (sqrt(V^) + eps) bends each column of M^ out of S; the modification    */
+/* makes the rate constant per column (the paper's "row-wise" mean), so a W   */
+/* whose columns lie in S stays there whenever the gradients' columns do, and */
+/* W_p2 needs no projection step.                                             */
+/*                                                                            */
+/*   M <- b1 M + (1 - b1) G          V <- b2 V + (1 - b2) G*G                 */
+/*   M^ = M / (1 - b1^t)             V^ = V / (1 - b2^t)                      */
+/*   subspace != 0:  alpha[:, c] = 1 / (sqrt(mean_r V^[r, c]) + eps)          */
+/*   subspace == 0:  alpha = 1 / (sqrt(V^) + eps) entrywise (standard AdamW)  */
+/*   W <- W - lr alpha M^ - weight_decay W                                    */
+/*                                                                            */
+/* The bias corrections are the usual 1 / (1 - beta^t) and the decay term is */
+/* weight_decay * W as the paper prints it (no lr factor).                    */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes of the subspace form for a rows x cols matrix (0 if
+ * invalid); the standard form needs none. */
+size_t sn_adamw_workspace_bytes(int64_t rows, int64_t cols);
+
+/* sn_adamw_step: one step, all arrays updated in place.
+ *
+ *   W       rows x cols weights (dt), row stride ldw >= cols, updated
+ *   G       rows x cols weight gradient (dt), row stride ldg >= cols, read
+ *   M, V    rows x cols first and second moments, float32, shared row stride
+ *           ldm >= cols, updated (zero before the first step)
+ *   t       step number, >= 1 (the bias corrections use it)
+ *   lr, beta1, beta2, eps, weight_decay: finite, lr, eps, weight_decay >= 0,
+ *           0 <= beta < 1
+ *   subspace   nonzero: column-constant rate (the modified step);
+ *              zero: the standard entrywise rate
+ *   workspace  sn_adamw_workspace_bytes(rows, cols) bytes, 256-byte aligned
+ *              (subspace form only; may be NULL otherwise)
+ * W, G, M, V and the workspace must not overlap.  rows == 0 or cols == 0 is a
+ * no-op.  Deterministic (fixed-order column sums).  Errors: NULL, SHAPE,
+ * DTYPE, ALIGN, ALIAS, WORKSPACE, HIP. */
+int32_t sn_adamw_step(void *W, int64_t ldw, const void *G, int64_t ldg, int32_t dt,
+                      float *M, float *V, int64_t ldm, int64_t rows, int64_t cols,
+                      int64_t t, double lr, double beta1, double beta2, double eps,
+                      double weight_decay, int32_t subspace,
+                      void *workspace, size_t workspace_bytes, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics.                                                               */
 /* ------------------------------------------------------------------------ */
 

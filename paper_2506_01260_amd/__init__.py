@@ -19,6 +19,8 @@ built the first call raises ``RuntimeError``.
     state = sn_grassmann_state(basis)                # subspace update (Sec. 4.5)
     Cg = sn_grassmann_accumulate(basis, G, state, want_cg=True)   # per iteration
     U2 = sn_grassmann_step(basis, state, eta)        # every few hundred iterations
+
+    sn_adamw_step(W2, grad, M, V, t, lr, weight_decay=wd)   # modified AdamW (Sec. 5)
 """
 from __future__ import annotations
 
@@ -65,6 +67,10 @@ _SIGNATURES = {
                                        _P, _SZ, _P]),
     "sn_grassmann_step": (_I32, [_P, _I64, _I64, _I32, _P, ctypes.c_double, _P, _I64, _I32, _P,
                                  _SZ, _P, _P]),
+    "sn_adamw_workspace_bytes": (_SZ, [_I64, _I64]),
+    "sn_adamw_step": (_I32, [_P, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _I64, _I64,
+                             ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                             ctypes.c_double, _I32, _P, _SZ, _P]),
     "sn_status_string": (ctypes.c_char_p, [_I32]),
     "sn_last_error": (ctypes.c_char_p, []),
     "sn_version": (ctypes.c_char_p, []),
@@ -426,6 +432,42 @@ def sn_grassmann_step(basis: Basis, state: GrassmannState, eta: float, out_dtype
                                    None if err_flag is None else err_flag.data_ptr(),
                                    _stream(stream)))
     return out
+
+
+def sn_adamw_workspace_bytes(rows: int, cols: int) -> int:
+    return lib().sn_adamw_workspace_bytes(rows, cols)
+
+
+def sn_adamw_step(W: torch.Tensor, G: torch.Tensor, M: torch.Tensor, V: torch.Tensor, t: int,
+                  lr: float, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+                  weight_decay: float = 0.0, subspace: bool = True, workspace=None,
+                  stream=None) -> torch.Tensor:
+    """One AdamW step in place on W (rows x cols, stored [out, in]) with fp32
+    moments M, V; subspace=True uses the column-constant rate of Sec. 5."""
+    wp, rows, cols, ldw = _mat(W, "W")
+    gp, gr, gc, ldg = _mat(G, "G")
+    mp, mr, mc, ldm = _mat(M, "M")
+    vp, vr, vc, ldv = _mat(V, "V")
+    if (gr, gc) != (rows, cols) or (mr, mc) != (rows, cols) or (vr, vc) != (rows, cols):
+        raise SnError(2, "W, G, M and V must have the same shape")
+    if ldv != ldm:
+        raise SnError(2, "M and V must share a row stride")
+    if M.dtype != torch.float32 or V.dtype != torch.float32:
+        raise SnError(3, "M and V must be float32")
+    dt = _dt(W)
+    if _dt(G) != dt:
+        raise SnError(3, "W and G must have the same dtype")
+    need = sn_adamw_workspace_bytes(rows, cols) if subspace else 0
+    if need and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=W.device)
+    if need and (workspace.numel() < need or not workspace.is_cuda):
+        raise SnError(9, f"workspace needs {need} device bytes")
+    _check(lib().sn_adamw_step(wp, ldw, gp, ldg, dt, mp, vp, ldm, rows, cols, int(t), float(lr),
+                               float(beta1), float(beta2), float(eps), float(weight_decay),
+                               1 if subspace else 0,
+                               workspace.data_ptr() if need else None, need,
+                               _stream(stream)))
+    return W
 
 
 def sn_version() -> str:

@@ -1,0 +1,241 @@
+// The modified AdamW step of Sec. 5 (and the standard step it modifies).
+//
+// W (rows x cols, stored [out, in]: the paper's W_p2 transposed, so the
+// paper's rows are the stored columns), its gradient G, first and second
+// moments M and V (fp32):
+//   M <- b1 M + (1 - b1) G,  V <- b2 V + (1 - b2) G^2
+//   M^ = M / (1 - b1^t),     V^ = V / (1 - b2^t)
+//   subspace:  alpha_c = 1 / (sqrt(mean over the column's rows of V^) + eps)
+//   standard:  alpha   = 1 / (sqrt(V^) + eps) entry by entry
+//   W <- W - lr alpha M^ - wd W
+// A column-constant alpha scales each column of M^ by one number, so a W
+// whose columns lie in S stays there when the gradients' columns do (Sec. 5,
+// App. A): no projection is needed for W_p2.
+//
+// Memory-bound.  A thread owns 8 consecutive columns (16-byte loads of bf16
+// G / W, 32-byte loads of M and V) over kRows rows.  Standard: one pass.
+// Subspace: pass 1 updates M and V and writes per-block column sums of V;
+// pass 2 adds the blocks in a fixed order and forms alpha; pass 3 reads M
+// again and updates W.
+#include "sn_device.h"
+#include "sn_internal.h"
+
+namespace sn {
+
+namespace {
+
+constexpr int kRows = 32;     // rows per thread
+constexpr int kCols = 8;      // columns per thread
+constexpr int kBlock = 128;   // threads per workgroup (1024 columns)
+
+struct AdamArgs {
+  float b1, omb1, b2, omb2;   // beta1, 1 - beta1, beta2, 1 - beta2
+  float inv_bc1, inv_bc2;     // 1 / (1 - beta^t)
+  float lr, eps, wd;
+};
+
+template <typename T> struct Vec8;
+template <> struct Vec8<bf16_t> {
+  static __device__ __forceinline__ void load(const bf16_t *p, float (&x)[8]) {
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = bf_lo(w[i]);
+      x[2 * i + 1] = bf_hi(w[i]);
+    }
+  }
+  static __device__ __forceinline__ void store(bf16_t *p, const float (&x)[8]) {
+    *reinterpret_cast<u32x4 *>(p) = u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                                          pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7])};
+  }
+};
+template <> struct Vec8<float> {
+  static __device__ __forceinline__ void load(const float *p, float (&x)[8]) {
+    const f32x4 a = *reinterpret_cast<const f32x4 *>(p);
+    const f32x4 b = *reinterpret_cast<const f32x4 *>(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  }
+  static __device__ __forceinline__ void store(float *p, const float (&x)[8]) {
+    *reinterpret_cast<f32x4 *>(p) = f32x4{x[0], x[1], x[2], x[3]};
+    *reinterpret_cast<f32x4 *>(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+  }
+};
+
+// 8 columns of one row: vector access when VEC (cols % 8 == 0, 16-byte
+// aligned rows), else element by element with a bound on the column
+template <typename T, bool VEC>
+__device__ __forceinline__ void load8(const T *row, int64_t c0, int64_t cols, float (&x)[8]) {
+  if constexpr (VEC) {
+    Vec8<T>::load(row + c0, x);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = c0 + i < cols ? to_f32(row[c0 + i]) : 0.0f;
+  }
+}
+
+template <typename T, bool VEC>
+__device__ __forceinline__ void store8(T *row, int64_t c0, int64_t cols, const float (&x)[8]) {
+  if constexpr (VEC) {
+    Vec8<T>::store(row + c0, x);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (c0 + i < cols) row[c0 + i] = from_f32<T>(x[i]);
+  }
+}
+
+// Pass 1 (and the whole standard step when !SUB): moments, then either the
+// column sums of the new V (SUB) or the W update with the entrywise rate.
+template <typename T, bool VEC, bool SUB>
+__global__ __launch_bounds__(kBlock) void moments_kernel(T *__restrict__ W, int64_t ldw,
+                                                         const T *__restrict__ G, int64_t ldg,
+                                                         float *__restrict__ M,
+                                                         float *__restrict__ V, int64_t ldm,
+                                                         int64_t rows, int64_t cols, AdamArgs a,
+                                                         float *__restrict__ colsum) {
+  const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kCols;
+  if (c0 >= cols) return;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kRows;
+  const int64_t r1 = r0 + kRows < rows ? r0 + kRows : rows;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int64_t r = r0; r < r1; ++r) {
+    float g[8], m[8], v[8];
+    load8<T, VEC>(G + r * ldg, c0, cols, g);
+    load8<float, VEC>(M + r * ldm, c0, cols, m);
+    load8<float, VEC>(V + r * ldm, c0, cols, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      m[i] = fmaf(a.b1, m[i], a.omb1 * g[i]);
+      v[i] = fmaf(a.b2, v[i], a.omb2 * (g[i] * g[i]));
+    }
+    store8<float, VEC>(M + r * ldm, c0, cols, m);
+    store8<float, VEC>(V + r * ldm, c0, cols, v);
+    if constexpr (SUB) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s[i] += v[i];
+    } else {
+      float w[8];
+      load8<T, VEC>(W + r * ldw, c0, cols, w);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float alpha = 1.0f / (sqrtf(v[i] * a.inv_bc2) + a.eps);
+        w[i] = w[i] - a.lr * alpha * (m[i] * a.inv_bc1) - a.wd * w[i];
+      }
+      store8<T, VEC>(W + r * ldw, c0, cols, w);
+    }
+  }
+  if constexpr (SUB) {
+    float *dst = colsum + static_cast<int64_t>(blockIdx.y) * cols;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (c0 + i < cols) dst[c0 + i] = s[i];
+  }
+}
+
+// Pass 2: alpha_c = 1 / (sqrt(sum_blocks colsum / (rows (1 - b2^t))) + eps),
+// the row blocks added in a fixed order in float64.
+__global__ __launch_bounds__(kBlock) void alpha_kernel(const float *__restrict__ colsum,
+                                                       int64_t nblk, int64_t rows, int64_t cols,
+                                                       double inv_bc2, double eps,
+                                                       float *__restrict__ alpha) {
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (c >= cols) return;
+  double s = 0.0;
+#pragma unroll 4
+  for (int64_t b = 0; b < nblk; ++b) s += static_cast<double>(colsum[b * cols + c]);
+  const double nu = s * inv_bc2 / static_cast<double>(rows);
+  alpha[c] = static_cast<float>(1.0 / (sqrt(nu) + eps));
+}
+
+// Pass 3: W <- W - lr alpha_c M^ - wd W with the column's rate.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(kBlock) void apply_kernel(T *__restrict__ W, int64_t ldw,
+                                                       const float *__restrict__ M, int64_t ldm,
+                                                       int64_t rows, int64_t cols, AdamArgs a,
+                                                       const float *__restrict__ alpha) {
+  const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kCols;
+  if (c0 >= cols) return;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kRows;
+  const int64_t r1 = r0 + kRows < rows ? r0 + kRows : rows;
+  float al[8];
+  load8<float, VEC>(alpha, c0, cols, al);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) al[i] *= a.lr * a.inv_bc1;
+#pragma unroll 4
+  for (int64_t r = r0; r < r1; ++r) {
+    float m[8], w[8];
+    load8<float, VEC>(M + r * ldm, c0, cols, m);
+    load8<T, VEC>(W + r * ldw, c0, cols, w);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = w[i] - al[i] * m[i] - a.wd * w[i];
+    store8<T, VEC>(W + r * ldw, c0, cols, w);
+  }
+}
+
+template <typename T, bool VEC>
+hipError_t launch_t(void *Wv, int64_t ldw, const void *Gv, int64_t ldg, float *M, float *V,
+                    int64_t ldm, int64_t rows, int64_t cols, const AdamArgs &a, double inv_bc2,
+                    double eps, bool sub, void *ws, hipStream_t s) {
+  T *W = static_cast<T *>(Wv);
+  const T *G = static_cast<const T *>(Gv);
+  const dim3 grid(static_cast<unsigned>(ceil_div(cols, kBlock * kCols)),
+                  static_cast<unsigned>(ceil_div(rows, kRows)));
+  if (!sub) {
+    moments_kernel<T, VEC, false><<<grid, kBlock, 0, s>>>(W, ldw, G, ldg, M, V, ldm, rows, cols,
+                                                          a, nullptr);
+    return hipGetLastError();
+  }
+  float *colsum = static_cast<float *>(ws);
+  float *alpha = colsum + static_cast<int64_t>(grid.y) * cols;
+  moments_kernel<T, VEC, true><<<grid, kBlock, 0, s>>>(W, ldw, G, ldg, M, V, ldm, rows, cols, a,
+                                                       colsum);
+  alpha_kernel<<<dim3(static_cast<unsigned>(ceil_div(cols, kBlock))), kBlock, 0, s>>>(
+      colsum, grid.y, rows, cols, inv_bc2, eps, alpha);
+  apply_kernel<T, VEC><<<grid, kBlock, 0, s>>>(W, ldw, M, ldm, rows, cols, a, alpha);
+  return hipGetLastError();
+}
+
+bool a16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+size_t adamw_workspace_bytes(int64_t rows, int64_t cols) {
+  // column sums per block of kRows rows, then the rates (fp32)
+  return align256(static_cast<size_t>(ceil_div(rows, kRows) + 1) * cols * sizeof(float));
+}
+
+hipError_t launch_adamw(int dt, void *W, int64_t ldw, const void *G, int64_t ldg, float *M,
+                        float *V, int64_t ldm, int64_t rows, int64_t cols, int64_t t, double lr,
+                        double beta1, double beta2, double eps, double wd, bool subspace,
+                        void *ws, hipStream_t s) {
+  const double bc1 = 1.0 - pow(beta1, static_cast<double>(t));
+  const double bc2 = 1.0 - pow(beta2, static_cast<double>(t));
+  AdamArgs a;
+  a.b1 = static_cast<float>(beta1);
+  a.omb1 = static_cast<float>(1.0 - beta1);
+  a.b2 = static_cast<float>(beta2);
+  a.omb2 = static_cast<float>(1.0 - beta2);
+  a.inv_bc1 = static_cast<float>(1.0 / bc1);
+  a.inv_bc2 = static_cast<float>(1.0 / bc2);
+  a.lr = static_cast<float>(lr);
+  a.eps = static_cast<float>(eps);
+  a.wd = static_cast<float>(wd);
+  const size_t es = dt == 0 ? 4 : 2;
+  const bool vec = cols % kCols == 0 && a16(W) && a16(G) && a16(M) && a16(V) &&
+                   (ldw * es) % 16 == 0 && (ldg * es) % 16 == 0 && (ldm * 4) % 16 == 0 &&
+                   a16(ws);
+  if (dt == 0)
+    return vec ? launch_t<float, true>(W, ldw, G, ldg, M, V, ldm, rows, cols, a, 1.0 / bc2, eps,
+                                       subspace, ws, s)
+               : launch_t<float, false>(W, ldw, G, ldg, M, V, ldm, rows, cols, a, 1.0 / bc2, eps,
+                                        subspace, ws, s);
+  return vec ? launch_t<bf16_t, true>(W, ldw, G, ldg, M, V, ldm, rows, cols, a, 1.0 / bc2, eps,
+                                      subspace, ws, s)
+             : launch_t<bf16_t, false>(W, ldw, G, ldg, M, V, ldm, rows, cols, a, 1.0 / bc2, eps,
+                                       subspace, ws, s);
+}
+
+}  // namespace sn

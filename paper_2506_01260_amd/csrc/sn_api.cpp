@@ -494,6 +494,51 @@ int32_t sn_grassmann_step(const void *basis, int64_t d, int64_t k, int32_t dt, c
                     "sn_grassmann_step launch");
 }
 
+size_t sn_adamw_workspace_bytes(int64_t rows, int64_t cols) {
+  if (rows < 0 || rows >= kMaxDim || cols < 0 || cols >= kMaxDim) return 0;
+  return sn::adamw_workspace_bytes(rows, cols);
+}
+
+int32_t sn_adamw_step(void *W, int64_t ldw, const void *G, int64_t ldg, int32_t dt, float *M,
+                      float *V, int64_t ldm, int64_t rows, int64_t cols, int64_t t, double lr,
+                      double beta1, double beta2, double eps, double weight_decay,
+                      int32_t subspace, void *workspace, size_t workspace_bytes,
+                      sn_stream stream) {
+  if (!dtype_ok(dt)) return fail(SN_ERR_DTYPE, "unknown dtype %d", dt);
+  if (rows < 0 || rows >= kMaxDim || cols < 0 || cols >= kMaxDim)
+    return fail(SN_ERR_SHAPE, "rows / cols out of range");
+  if (t < 1) return fail(SN_ERR_SHAPE, "t counts steps from 1 (t = %lld)", (long long)t);
+  if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+    return fail(SN_ERR_SHAPE, "betas must lie in [0, 1)");
+  if (!(eps >= 0.0 && eps <= 1e30) || !(lr >= 0.0 && lr <= 1e30) ||
+      !(weight_decay >= 0.0 && weight_decay <= 1e30))
+    return fail(SN_ERR_SHAPE, "lr, eps and weight_decay must be finite and >= 0");
+  if (rows == 0 || cols == 0) return ok();
+  if (ldw < cols || ldg < cols || ldm < cols || ldw >= kMaxDim || ldg >= kMaxDim ||
+      ldm >= kMaxDim)
+    return fail(SN_ERR_SHAPE, "row strides must be >= cols");
+  if (!W || !G || !M || !V) return fail(SN_ERR_NULL, "W, G, M and V are required");
+  if (!elem_aligned(W, dt) || !elem_aligned(G, dt) || !elem_aligned(M, SN_F32) ||
+      !elem_aligned(V, SN_F32))
+    return fail(SN_ERR_ALIGN, "W, G, M or V not aligned to its element size");
+  int32_t st;
+  const size_t need = subspace ? sn_adamw_workspace_bytes(rows, cols) : 0;
+  if (subspace && (st = check_workspace(workspace, workspace_bytes, need))) return st;
+  const size_t es = elem_size(dt);
+  const Span w = span(W, rows, cols, ldw, es), g = span(G, rows, cols, ldg, es);
+  const Span m = span(M, rows, cols, ldm, 4), v = span(V, rows, cols, ldm, 4);
+  const Span ws = subspace ? bytes_span(workspace, need) : Span{};
+  const Span all[5] = {w, g, m, v, ws};
+  for (int i = 0; i < 5; ++i)
+    for (int j = i + 1; j < 5; ++j)
+      if (overlap(all[i], all[j]))
+        return fail(SN_ERR_ALIAS, "W, G, M, V and the workspace must not overlap");
+  return hip_status(sn::launch_adamw(dt, W, ldw, G, ldg, M, V, ldm, rows, cols, t, lr, beta1,
+                                     beta2, eps, weight_decay, subspace != 0, workspace,
+                                     static_cast<hipStream_t>(stream)),
+                    "sn_adamw_step launch");
+}
+
 const char *sn_status_string(int32_t status) {
   switch (status) {
     case SN_OK: return "SN_OK";

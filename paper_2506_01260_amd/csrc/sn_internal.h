@@ -149,6 +149,13 @@ hipError_t launch_grass_reset(void *state, int64_t d, int64_t k, hipStream_t s);
 hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, const void *G,
                                    int64_t N, int64_t ldg, void *Cwire, int64_t ldc, bool with_su,
                                    void *state, void *ws, hipStream_t s);
+// ---- modified AdamW (Sec. 5) ---------------------------------------------------
+size_t adamw_workspace_bytes(int64_t rows, int64_t cols);
+hipError_t launch_adamw(int dt, void *W, int64_t ldw, const void *G, int64_t ldg, float *M,
+                        float *V, int64_t ldm, int64_t rows, int64_t cols, int64_t t, double lr,
+                        double beta1, double beta2, double eps, double wd, bool subspace,
+                        void *ws, hipStream_t s);
+
 hipError_t launch_grass_step(const PackLayout &L, const void *packed, const void *state,
                              double eta, void *Unew, int64_t ldu, int out_dt, void *ws,
                              int32_t *err_flag, hipStream_t s);

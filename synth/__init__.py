@@ -6,7 +6,8 @@ projection routine and nothing here is ever used to produce an expected value.
 
 Every tensor is drawn on the host with numpy ``Generator(PCG64(seed))`` where
 ``seed = 1260 + 100 * cfg + ordinal`` (ordinal: 0 U, 1 E, 2 P, 3 tok,
-4 C_true, 5 noise, 6 G, 7 + i weight matrix i, 79 the dominant gradient
+4 C_true, 5 noise, 6 G, 7 + i weight matrix i, 71 / 72 the AdamW moments,
+73 + t the weight gradient of optimizer step t, 79 the dominant gradient
 directions and 80 + t the gradient of iteration t of the subspace update).  Large tensors are drawn in
 fixed row blocks of ``ROW_BLOCK`` rows, block b using ``SeedSequence([seed, b])``,
 so a tensor's values do not depend on how callers slice it.
@@ -64,6 +65,8 @@ CONFIGS = {
 }
 
 ORD_U, ORD_E, ORD_P, ORD_TOK, ORD_C, ORD_NOISE, ORD_G, ORD_W = range(8)
+ORD_AM, ORD_AV = 71, 72   # AdamW moments M, V of the optimizer-step inputs
+ORD_AG = 73        # 73 + t: weight gradient of optimizer step t (t < 6)
 ORD_GV = 79        # fixed dominant gradient directions of the subspace-update inputs
 ORD_GT = 80        # 80 + t: activation gradient of accumulated iteration t (t < 20)
 
@@ -286,6 +289,31 @@ def make_grad_iteration(cfg_id: int, t: int, n: int | None = None, cfg: Config |
 
     _parallel(one, _blocks(n))
     return out
+
+
+def make_adamw_state(cfg_id: int, rows: int, cols: int, scale: float = 1e-3) -> dict:
+    """Float32 AdamW moments of a weight mid-training: M ~ N(0, scale^2) and
+    V = (|N(0, 1)| scale + scale / 10)^2 (positive, varying across entries)."""
+    M = gaussian(seed_of(cfg_id, ORD_AM), rows, cols, scale)
+    a = gaussian(seed_of(cfg_id, ORD_AV), rows, cols, scale)
+    V = (np.abs(a) + np.float32(scale / 10)) ** 2
+    return {"M": M, "V": V.astype(np.float32)}
+
+
+def make_weight_grad(cfg_id: int, t: int, rows: int, cols: int, cfg: Config | None = None,
+                     scale: float = 1e-3, basis: np.ndarray | None = None) -> np.ndarray:
+    """Weight gradient of optimizer step t, N(0, scale^2) with a per-column
+    scale in [0.1, 10] (uneven second moments across columns), stored in the
+    config's dtype; with `basis` (d x k, float64) the columns are projected
+    onto its span first (gradients confined to S, Sec. 5 and App. A)."""
+    cfg = cfg or CONFIGS[cfg_id]
+    if not 0 <= t < 6:
+        raise ValueError("t must be in [0, 6)")
+    g = gaussian(seed_of(cfg_id, ORD_AG + t), rows, cols, scale).astype(np.float64)
+    g *= _rng(seed_of(cfg_id, ORD_AG + t), 1 << 20).uniform(0.1, 10.0, size=(1, cols))
+    if basis is not None:
+        g = basis @ (basis.T @ g)
+    return store(g, cfg.dtype)
 
 
 def make_weight(cfg_id: int, index: int, rows: int, cols: int,

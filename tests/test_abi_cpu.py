@@ -209,3 +209,28 @@ def test_grassmann_sizes_and_validation():
     assert L.sn_grassmann_reset(None, 256, 8, None) == 1
     assert L.sn_grassmann_reset(state + 64, 256, 8, None) == 4
     assert L.sn_grassmann_reset(state, 256, 300, None) == 2
+
+
+def test_adamw_sizes_and_validation():
+    L = sn.lib()
+    assert L.sn_adamw_workspace_bytes(4096, 14336) >= (4096 // 64 + 1) * 14336 * 4
+    assert L.sn_adamw_workspace_bytes(-1, 8) == 0
+    W, G, M, V, w = (FAKE + (i << 24) for i in range(1, 6))
+    need = L.sn_adamw_workspace_bytes(64, 32)
+
+    def step(**over):
+        a = dict(W=W, ldw=32, G=G, ldg=32, dt=1, M=M, V=V, ldm=32, rows=64, cols=32, t=1,
+                 lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, wd=0.0, sub=1, ws=w, nbytes=need)
+        a.update(over)
+        return L.sn_adamw_step(a["W"], a["ldw"], a["G"], a["ldg"], a["dt"], a["M"], a["V"],
+                               a["ldm"], a["rows"], a["cols"], a["t"], a["lr"], a["b1"], a["b2"],
+                               a["eps"], a["wd"], a["sub"], a["ws"], a["nbytes"], None)
+    assert step(dt=4) == 3
+    assert step(t=0) == 2 and step(b1=1.0) == 2 and step(b2=-0.1) == 2
+    assert step(lr=float("nan")) == 2 and step(eps=-1.0) == 2 and step(wd=float("inf")) == 2
+    assert step(ldw=16) == 2 and step(ldm=31) == 2
+    assert step(W=None) == 1 and step(M=None) == 1
+    assert step(W=W + 1) == 4 and step(M=M + 2) == 4
+    assert step(ws=None) == 1 and step(nbytes=need - 1) == 9 and step(ws=w + 64) == 4
+    assert step(G=W) == 5 and step(V=M + 64) == 5 and step(ws=V) == 5
+    assert step(rows=0, W=None, G=None) == 0
