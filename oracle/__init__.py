@@ -17,7 +17,8 @@ the output dtype with round-to-nearest-even:
 
 The subspace update of Section 4.5 (off-subspace loss, accumulation matrix,
 Riemannian gradient, QR retraction) is in ``grassmann``; the modified AdamW
-step of Section 5 in ``adamw``.
+step of Section 5 in ``adamw``; the trainable low-rank token table of
+Section 4.3.1 in ``embed``.
 
 ``exact`` holds the same operations in exact rational arithmetic
 (``fractions.Fraction``) for brute-force checks on tiny inputs.
@@ -25,8 +26,8 @@ step of Section 5 in ``adamw``.
 from .bf16 import decode_bf16, encode_bf16, round_bf16, round_f32, round_to
 from .codec import (compress, decompress, grad_compress, grad_decompress,
                     project_weights, default_positions)
-from . import adamw, grassmann
+from . import adamw, embed, grassmann
 
 __all__ = ["decode_bf16", "encode_bf16", "round_bf16", "round_f32", "round_to",
            "compress", "decompress", "grad_compress", "grad_decompress",
-           "project_weights", "default_positions", "grassmann", "adamw"]
+           "project_weights", "default_positions", "grassmann", "adamw", "embed"]
