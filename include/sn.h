@@ -296,6 +296,62 @@ int32_t sn_grassmann_step(const void *basis, int64_t d, int64_t k, int32_t dt,
                           sn_stream stream);
 
 /* ------------------------------------------------------------------------ */
+/* Trainable low-rank token table (Sec. 4.3.1).                               */
+/*                                                                            */
+/* TE = T_fixed[t] + T_S[t], T_S = T_fixed U U^T at the start of training.    */
+/* T_S is kept as its coefficients C_S (vocab x k, element type dt):          */
+/* T_S = C_S U^T, so its rows lie in S whatever update C_S receives, and the  */
+/* codec's compress of an activation carries T_S[t] inside C (Eq. subtract    */
+/* subtracts only PE and T_fixed).  C_S's initial value T_fixed U is          */
+/* sn_grad_compress applied to T_fixed (vocab rows).  After a subspace update */
+/* (U -> U'), C_S' = (C_S U^T) U' keeps the part of T_S that lies in the new  */
+/* subspace: sn_decompress with the old basis, then sn_grad_compress with     */
+/* the new one.                                                               */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes of the forward and backward calls for N tokens (0 if
+ * invalid). */
+size_t sn_embed_lowrank_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t N,
+                                        int64_t vocab);
+
+/* sn_embed_lowrank_forward: X0[i, :] = P[pos_i, :] + E[tok_i, :] + C_S[tok_i, :] U^T
+ * (the embedding output PE + TE of Sec. 4.2 with the decomposed table).
+ *
+ *   CS         vocab x k coefficients of T_S (dt), row stride ldcs >= k
+ *   tok        int32[N] token ids (required); out-of-range ids are clamped and
+ *              reported in bit 0 of *err_flag
+ *   E          vocab x d T_fixed (row stride lde >= d), or NULL: no fixed term
+ *   pos, P, n_pos, ldp, seq_len: as in sn_decompress
+ *   X0         N x d output (dt), row stride ldx >= d
+ *   workspace  sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab) bytes,
+ *              256-byte aligned
+ * Errors: NULL, SHAPE, DTYPE, ALIGN, ALIAS, WORKSPACE, UNSUPPORTED, HIP. */
+int32_t sn_embed_lowrank_forward(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                 const void *CS, int64_t vocab, int64_t ldcs,
+                                 const int32_t *tok, const void *E, int64_t lde,
+                                 const int32_t *pos, const void *P, int64_t n_pos, int64_t ldp,
+                                 int64_t seq_len, void *X0, int64_t N, int64_t ldx,
+                                 int32_t *err_flag, void *workspace, size_t workspace_bytes,
+                                 sn_stream stream);
+
+/* sn_embed_lowrank_backward: gCS[v, :] += sum over i with tok_i = v of dX0[i, :] U
+ * (the gradient of C_S given the gradient dX0 of the embedding output: the
+ * lookup's scatter, through T_S = C_S U^T).
+ *
+ *   dX0   N x d gradient (dt), row stride ldg >= d
+ *   tok   int32[N] token ids (clamped, bit 0 of *err_flag)
+ *   gCS   vocab x k float32 gradient, row stride ldgc >= k, ACCUMULATED into
+ *         (rows of ids that do not occur are untouched)
+ *   workspace  sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab) bytes
+ * Deterministic: the rows of each id are summed in ascending token order in
+ * float64 (a stable counting sort by id runs in one workgroup).  Errors:
+ * NULL, SHAPE, DTYPE, ALIGN, ALIAS, WORKSPACE, UNSUPPORTED, HIP. */
+int32_t sn_embed_lowrank_backward(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                  const void *dX0, int64_t N, int64_t ldg, const int32_t *tok,
+                                  int64_t vocab, float *gCS, int64_t ldgc, int32_t *err_flag,
+                                  void *workspace, size_t workspace_bytes, sn_stream stream);
+
+/* ------------------------------------------------------------------------ */
 /* Modified AdamW (Sec. 5).                                                   */
 /*                                                                            */
 /* W_p2's rows lie in S in the paper's layout; stored [out, in] (d x m, as    */

@@ -67,6 +67,11 @@ _SIGNATURES = {
                                        _P, _SZ, _P]),
     "sn_grassmann_step": (_I32, [_P, _I64, _I64, _I32, _P, ctypes.c_double, _P, _I64, _I32, _P,
                                  _SZ, _P, _P]),
+    "sn_embed_lowrank_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64, _I64]),
+    "sn_embed_lowrank_forward": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _P, _I64, _P,
+                                        _P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _SZ, _P]),
+    "sn_embed_lowrank_backward": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _I64, _P,
+                                         _I64, _P, _P, _SZ, _P]),
     "sn_adamw_workspace_bytes": (_SZ, [_I64, _I64]),
     "sn_adamw_step": (_I32, [_P, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _I64, _I64,
                              ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
@@ -432,6 +437,61 @@ def sn_grassmann_step(basis: Basis, state: GrassmannState, eta: float, out_dtype
                                    None if err_flag is None else err_flag.data_ptr(),
                                    _stream(stream)))
     return out
+
+
+def sn_embed_lowrank_workspace_bytes(d: int, k: int, dt: int, N: int, vocab: int) -> int:
+    return lib().sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab)
+
+
+def sn_embed_lowrank_forward(basis: Basis, CS: torch.Tensor, tok: torch.Tensor, E=None, P=None,
+                             pos=None, seq_len=None, out=None, err_flag=None, workspace=None,
+                             stream=None) -> torch.Tensor:
+    """X0 = P[pos] + E[tok] + CS[tok] U^T (the low-rank token table T_S = CS U^T)."""
+    cp, vocab, k, ldcs = _mat(CS, "CS")
+    if k != basis.k:
+        raise SnError(2, f"CS has {k} columns, basis has k = {basis.k}")
+    N = tok.shape[0]
+    _same_d(basis, basis.d, ("E", E), ("P", P))
+    if E is not None and E.shape[0] != vocab:
+        raise SnError(2, "E and CS must have the same number of rows")
+    if out is None:
+        out = torch.empty((N, basis.d), dtype=_torch_dtype(basis.dt), device=CS.device)
+    _out_shape(out, (N, basis.d), "out")
+    _same_dtype(basis, ("CS", CS), ("E", E), ("P", P), ("out", out))
+    xp, _, _, ldx = _mat(out, "out")
+    tok_ptr = _ids(tok, "tok", N)
+    _, e_ptr, _, lde, pos_ptr, p_ptr, n_pos, ldp, sl = _tables(N, tok, E, pos, P, seq_len)
+    need = sn_embed_lowrank_workspace_bytes(basis.d, basis.k, basis.dt, N, vocab)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=CS.device)
+    _check(lib().sn_embed_lowrank_forward(basis.ptr, basis.d, basis.k, basis.dt, cp, vocab, ldcs,
+                                          tok_ptr, e_ptr, lde, pos_ptr, p_ptr, n_pos, ldp, sl,
+                                          xp, N, ldx,
+                                          None if err_flag is None else err_flag.data_ptr(),
+                                          workspace.data_ptr(), workspace.numel(),
+                                          _stream(stream)))
+    return out
+
+
+def sn_embed_lowrank_backward(basis: Basis, dX0: torch.Tensor, tok: torch.Tensor, gCS: torch.Tensor,
+                              err_flag=None, workspace=None, stream=None) -> torch.Tensor:
+    """gCS += scatter over tok of dX0 U (float32 gCS, vocab x k); returns gCS."""
+    gp, N, d, ldg = _mat(dX0, "dX0")
+    _same_d(basis, d)
+    _same_dtype(basis, ("dX0", dX0))
+    cp, vocab, k, ldgc = _mat(gCS, "gCS")
+    if k != basis.k or gCS.dtype != torch.float32:
+        raise SnError(2, f"gCS must be float32 with k = {basis.k} columns")
+    tok_ptr = _ids(tok, "tok", N)
+    need = sn_embed_lowrank_workspace_bytes(basis.d, basis.k, basis.dt, N, vocab)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dX0.device)
+    _check(lib().sn_embed_lowrank_backward(basis.ptr, basis.d, basis.k, basis.dt, gp, N, ldg,
+                                           tok_ptr, vocab, cp, ldgc,
+                                           None if err_flag is None else err_flag.data_ptr(),
+                                           workspace.data_ptr(), workspace.numel(),
+                                           _stream(stream)))
+    return gCS
 
 
 def sn_adamw_workspace_bytes(rows: int, cols: int) -> int:

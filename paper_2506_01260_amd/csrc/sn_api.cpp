@@ -494,6 +494,79 @@ int32_t sn_grassmann_step(const void *basis, int64_t d, int64_t k, int32_t dt, c
                     "sn_grassmann_step launch");
 }
 
+size_t sn_embed_lowrank_workspace_bytes(int64_t d, int64_t k, int32_t dt, int64_t N,
+                                        int64_t vocab) {
+  if (!dtype_ok(dt) || d < 1 || d >= kMaxDim || k < 1 || k > d || k > SN_MAX_K || N < 0 ||
+      N >= kMaxDim || vocab < 1 || vocab >= kMaxDim)
+    return 0;
+  return sn::embed_workspace_bytes(k, dt, N, vocab);
+}
+
+int32_t sn_embed_lowrank_forward(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                 const void *CS, int64_t vocab, int64_t ldcs, const int32_t *tok,
+                                 const void *E, int64_t lde, const int32_t *pos, const void *P,
+                                 int64_t n_pos, int64_t ldp, int64_t seq_len, void *X0,
+                                 int64_t N, int64_t ldx, int32_t *err_flag, void *workspace,
+                                 size_t workspace_bytes, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (N < 0 || N >= kMaxDim) return fail(SN_ERR_SHAPE, "N out of range");
+  if (vocab < 1 || vocab >= kMaxDim) return fail(SN_ERR_SHAPE, "vocab out of range");
+  if (ldcs < k || ldcs >= kMaxDim) return fail(SN_ERR_SHAPE, "ldcs must be >= k");
+  if (ldx < d || ldx >= kMaxDim) return fail(SN_ERR_SHAPE, "ldx must be >= d");
+  if ((st = check_ids(N, d, dt, tok, E, vocab, lde, pos, P, n_pos, ldp, seq_len))) return st;
+  if (N == 0) return ok();
+  if (!CS || !tok || !X0) return fail(SN_ERR_NULL, "CS, tok and X0 are required");
+  if (!elem_aligned(CS, dt) || !elem_aligned(X0, dt) || (reinterpret_cast<uintptr_t>(tok) & 3))
+    return fail(SN_ERR_ALIGN, "CS, X0 or tok misaligned");
+  const size_t need = sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab);
+  if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
+  const size_t es = elem_size(dt);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  const Span x = span(X0, N, d, ldx, es), w = bytes_span(workspace, need);
+  if ((st = check_out_alias(x, basis, L.total, span(CS, vocab, k, ldcs, es), N, tok, E, vocab,
+                            lde, pos, P, n_pos, ldp, d, es)))
+    return st;
+  if (overlap(x, span(tok, 1, N, N, 4)) || overlap(x, w) || overlap(w, span(CS, vocab, k, ldcs, es)) ||
+      overlap(w, span(tok, 1, N, N, 4)) || overlap(w, bytes_span(basis, L.total)) ||
+      (E && overlap(w, span(E, vocab, d, lde, es))) || (P && overlap(w, span(P, n_pos, d, ldp, es))))
+    return fail(SN_ERR_ALIAS, "X0 or the workspace overlaps an input");
+  const sn::IdArgs ids = make_ids(tok, E, vocab, lde, pos, P, n_pos, ldp, seq_len, err_flag);
+  return hip_status(sn::launch_embed_forward(L, basis, CS, vocab, ldcs, tok, ids, N, X0, ldx,
+                                             workspace, static_cast<hipStream_t>(stream)),
+                    "sn_embed_lowrank_forward launch");
+}
+
+int32_t sn_embed_lowrank_backward(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                  const void *dX0, int64_t N, int64_t ldg, const int32_t *tok,
+                                  int64_t vocab, float *gCS, int64_t ldgc, int32_t *err_flag,
+                                  void *workspace, size_t workspace_bytes, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (N < 0 || N >= kMaxDim) return fail(SN_ERR_SHAPE, "N out of range");
+  if (vocab < 1 || vocab >= kMaxDim) return fail(SN_ERR_SHAPE, "vocab out of range");
+  if (ldg < d || ldg >= kMaxDim) return fail(SN_ERR_SHAPE, "ldg must be >= d");
+  if (ldgc < k || ldgc >= kMaxDim) return fail(SN_ERR_SHAPE, "ldgc must be >= k");
+  if (N == 0) return ok();
+  if (!dX0 || !tok || !gCS) return fail(SN_ERR_NULL, "dX0, tok and gCS are required");
+  if (!elem_aligned(dX0, dt) || !elem_aligned(gCS, SN_F32) ||
+      (reinterpret_cast<uintptr_t>(tok) & 3))
+    return fail(SN_ERR_ALIGN, "dX0, gCS or tok misaligned");
+  const size_t need = sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab);
+  if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  const Span g = span(gCS, vocab, k, ldgc, 4), w = bytes_span(workspace, need);
+  const Span x = span(dX0, N, d, ldg, elem_size(dt)), t = span(tok, 1, N, N, 4);
+  const Span b = bytes_span(basis, L.total);
+  if (overlap(g, x) || overlap(g, t) || overlap(g, w) || overlap(g, b) || overlap(w, x) ||
+      overlap(w, t) || overlap(w, b))
+    return fail(SN_ERR_ALIAS, "gCS, the workspace and the inputs must not overlap");
+  return hip_status(sn::launch_embed_backward(L, basis, dX0, N, ldg, tok, vocab, gCS, ldgc,
+                                              err_flag, workspace,
+                                              static_cast<hipStream_t>(stream)),
+                    "sn_embed_lowrank_backward launch");
+}
+
 size_t sn_adamw_workspace_bytes(int64_t rows, int64_t cols) {
   if (rows < 0 || rows >= kMaxDim || cols < 0 || cols >= kMaxDim) return 0;
   return sn::adamw_workspace_bytes(rows, cols);

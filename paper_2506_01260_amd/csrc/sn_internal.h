@@ -149,6 +149,17 @@ hipError_t launch_grass_reset(void *state, int64_t d, int64_t k, hipStream_t s);
 hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, const void *G,
                                    int64_t N, int64_t ldg, void *Cwire, int64_t ldc, bool with_su,
                                    void *state, void *ws, hipStream_t s);
+// ---- low-rank token table (Sec. 4.3.1) -------------------------------------------
+size_t embed_workspace_bytes(int64_t k, int dt, int64_t N, int64_t vocab);
+hipError_t launch_embed_forward(const PackLayout &L, const void *packed, const void *CS,
+                                int64_t vocab, int64_t ldcs, const int32_t *tok,
+                                const IdArgs &ids, int64_t N, void *X0, int64_t ldx, void *ws,
+                                hipStream_t s);
+hipError_t launch_embed_backward(const PackLayout &L, const void *packed, const void *dX0,
+                                 int64_t N, int64_t ldg, const int32_t *tok, int64_t vocab,
+                                 float *gCS, int64_t ldgc, int32_t *err_flag, void *ws,
+                                 hipStream_t s);
+
 // ---- modified AdamW (Sec. 5) ---------------------------------------------------
 size_t adamw_workspace_bytes(int64_t rows, int64_t cols);
 hipError_t launch_adamw(int dt, void *W, int64_t ldw, const void *G, int64_t ldg, float *M,

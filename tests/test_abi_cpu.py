@@ -234,3 +234,36 @@ def test_adamw_sizes_and_validation():
     assert step(ws=None) == 1 and step(nbytes=need - 1) == 9 and step(ws=w + 64) == 4
     assert step(G=W) == 5 and step(V=M + 64) == 5 and step(ws=V) == 5
     assert step(rows=0, W=None, G=None) == 0
+
+
+def test_embed_lowrank_validation():
+    L = sn.lib()
+    need = L.sn_embed_lowrank_workspace_bytes(256, 8, 1, 512, 100)
+    assert need > 512 * 16 * 4 and L.sn_embed_lowrank_workspace_bytes(256, 8, 1, 512, 0) == 0
+    CS, tok, E, X0, w, g = (FAKE + (i << 24) for i in range(1, 7))
+
+    def fwd(**over):
+        a = dict(CS=CS, vocab=100, ldcs=8, tok=tok, E=E, lde=256, X0=X0, N=512, ldx=256, ws=w,
+                 nbytes=need)
+        a.update(over)
+        return L.sn_embed_lowrank_forward(FAKE, 256, 8, 1, a["CS"], a["vocab"], a["ldcs"],
+                                          a["tok"], a["E"], a["lde"], None, None, 0, 0, 0,
+                                          a["X0"], a["N"], a["ldx"], None, a["ws"], a["nbytes"],
+                                          None)
+    assert fwd(CS=None) == 1 and fwd(tok=None) == 1 and fwd(X0=None) == 1
+    assert fwd(ldcs=4) == 2 and fwd(ldx=100) == 2 and fwd(vocab=0) == 2
+    assert fwd(nbytes=need - 1) == 9 and fwd(ws=w + 8) == 4
+    assert fwd(X0=CS) == 5 and fwd(ws=X0) == 5
+    assert fwd(N=0, X0=None) == 0
+
+    def bwd(**over):
+        a = dict(dX=X0, N=512, ldg=256, tok=tok, vocab=100, g=g, ldgc=8, ws=w, nbytes=need)
+        a.update(over)
+        return L.sn_embed_lowrank_backward(FAKE, 256, 8, 1, a["dX"], a["N"], a["ldg"], a["tok"],
+                                           a["vocab"], a["g"], a["ldgc"], None, a["ws"],
+                                           a["nbytes"], None)
+    assert bwd(dX=None) == 1 and bwd(g=None) == 1 and bwd(tok=None) == 1
+    assert bwd(ldg=10) == 2 and bwd(ldgc=7) == 2 and bwd(vocab=0) == 2
+    assert bwd(g=g + 2) == 4 and bwd(nbytes=need - 1) == 9
+    assert bwd(g=X0) == 5 and bwd(ws=tok) == 5
+    assert bwd(N=0, dX=None) == 0
