@@ -61,6 +61,10 @@ OP_KERNELS = {
 
 # kernels that only the subspace update launches
 GRASS_KERNELS = ["loss_kernel", "frag_kernel", "finish_kernel", "gram_partial_kernel", "gram_reduce_kernel",
+                 "moments_kernel", "alpha_kernel", "apply_kernel", "gather_rows_kernel",
+                 "zero_kernel", "hist_kernel", "block_prefix_kernel", "tile_scan_kernel",
+                 "tiles_scan_kernel", "tile_write_kernel", "place_kernel",
+                 "chunk_sum_kernel", "seg_sum_kernel",
                  "update_kernel", "chol_kernel", "tri_apply_kernel", "reset_kernel",
                  "compress_kernel<3, false, false, false, 3>"]
 
@@ -285,7 +289,7 @@ def trace_summary(trace_dir: str, bench_log: str):
     grass = [i for i in range(at, len(rows))
              if names[i] in GRASS_KERNELS or names[i].split("<")[0] in GRASS_KERNELS]
     if grass:
-        cuts.append(("subspace update (accumulate, monitor, step; warm-up included)", at,
+        cuts.append(("subspace update, AdamW, low-rank table (warm-up included)", at,
                      grass[-1] + 1))
         at = grass[-1] + 1
     if at < len(rows):
@@ -578,6 +582,51 @@ def adamw_times(sn, torch, weights, steps: int) -> dict:
     return out
 
 
+def embed_times(sn, torch, basis, w, d: int, k: int, N: int, steps: int) -> dict:
+    """The low-rank token table of Sec. 4.3.1 at the step's shape: the
+    forward X0 = P + T_fixed[t] + C_S[t] U^T and the backward gC_S +=
+    scatter(dX0 U), mean ms per call."""
+    cfg = w["cfg"]
+    E, P = to_dev(w["E"]), to_dev(w["P"])
+    tok = torch.from_numpy(w["tok"]).cuda()
+    CS = sn.sn_grad_compress(basis, E)                   # C_S = T_fixed U
+    X0 = torch.empty(N, d, dtype=torch.bfloat16, device="cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(11)
+    dX = (torch.randn(N, d, device="cuda", generator=gen) * 1e-2).to(torch.bfloat16)
+    gCS = torch.zeros(cfg.vocab, k, device="cuda")
+    wsb = sn.sn_embed_lowrank_workspace_bytes(d, k, basis.dt, N, cfg.vocab)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    fwd = timed(lambda: sn.sn_embed_lowrank_forward(basis, CS, tok, E=E, P=P, seq_len=cfg.seq,
+                                                    out=X0, workspace=ws))
+    bwd = timed(lambda: sn.sn_embed_lowrank_backward(basis, dX, tok, gCS, workspace=ws))
+    uniq = len(np.unique(w["tok"]))
+    # forward: X0 written, the batch's unique T_fixed rows and C_S rows, P, U once
+    fbytes = N * d * 2 + uniq * (d + k) * 2 + min(cfg.seq, N) * d * 2 + d * k * 2
+    # backward: dX0 read, the unique gC_S rows read and written, U
+    bbytes = N * d * 2 + 2 * uniq * k * 4 + d * k * 2
+    del E, P, X0, dX, gCS, ws, CS
+    torch.cuda.empty_cache()
+    return {"forward_ms": round(fwd, 5), "forward_bytes": fbytes,
+            "forward_GBps": round(fbytes / (fwd * 1e-3) / 1e9, 1),
+            "backward_ms": round(bwd, 5), "backward_bytes": bbytes,
+            "backward_GBps": round(bbytes / (bwd * 1e-3) / 1e9, 1)}
+
+
 def load_traffic():
     try:
         t = json.load(open(TRAFFIC_FILE))
@@ -855,6 +904,8 @@ def main():
     print("[bench] subspace update timed", file=sys.stderr, flush=True)
     out["adamw"] = adamw_times(sn, torch, weights, K)
     print("[bench] AdamW timed", file=sys.stderr, flush=True)
+    out["embed_lowrank"] = embed_times(sn, torch, basis, w, d, k, N, K)
+    print("[bench] low-rank token table timed", file=sys.stderr, flush=True)
     if not args.no_other_configs:
         del Xs, Gs, Cs, Cgs, Cps, Xrs, Grs, weights
         torch.cuda.empty_cache()

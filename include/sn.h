@@ -339,12 +339,12 @@ int32_t sn_embed_lowrank_forward(const void *basis, int64_t d, int64_t k, int32_
  * lookup's scatter, through T_S = C_S U^T).
  *
  *   dX0   N x d gradient (dt), row stride ldg >= d
- *   tok   int32[N] token ids (clamped, bit 0 of *err_flag)
+ *   tok   int32[N] token ids (clamped, bit 0 of *err_flag); vocab < 2^21
  *   gCS   vocab x k float32 gradient, row stride ldgc >= k, ACCUMULATED into
  *         (rows of ids that do not occur are untouched)
  *   workspace  sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab) bytes
  * Deterministic: the rows of each id are summed in ascending token order in
- * float64 (a stable counting sort by id runs in one workgroup).  Errors:
+ * float64 (after a stable counting sort of the token indices by id).  Errors:
  * NULL, SHAPE, DTYPE, ALIGN, ALIAS, WORKSPACE, UNSUPPORTED, HIP. */
 int32_t sn_embed_lowrank_backward(const void *basis, int64_t d, int64_t k, int32_t dt,
                                   const void *dX0, int64_t N, int64_t ldg, const int32_t *tok,

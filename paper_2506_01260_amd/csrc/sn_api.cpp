@@ -547,6 +547,9 @@ int32_t sn_embed_lowrank_backward(const void *basis, int64_t d, int64_t k, int32
   if (vocab < 1 || vocab >= kMaxDim) return fail(SN_ERR_SHAPE, "vocab out of range");
   if (ldg < d || ldg >= kMaxDim) return fail(SN_ERR_SHAPE, "ldg must be >= d");
   if (ldgc < k || ldgc >= kMaxDim) return fail(SN_ERR_SHAPE, "ldgc must be >= k");
+  if (vocab >= (int64_t(1) << 21))
+    return fail(SN_ERR_UNSUPPORTED, "the gradient scatter sorts ids below 2^21 (vocab = %lld)",
+                (long long)vocab);
   if (N == 0) return ok();
   if (!dX0 || !tok || !gCS) return fail(SN_ERR_NULL, "dX0, tok and gCS are required");
   if (!elem_aligned(dX0, dt) || !elem_aligned(gCS, SN_F32) ||

@@ -8,11 +8,13 @@
 //           recovery with C = C_S[tok]).
 // backward  gC_S[v] += sum over i with tok_i = v of dX0[i] U: the gradient
 //           coefficients dX0 U in fp32 (the compress kernel's fp32-row
-//           epilogue), then a deterministic segmented sum by token id:
-//           a one-workgroup stable counting sort of the token indices
-//           (segments of equal ids, indices ascending), per-chunk sums of at
-//           most 64 rows of a segment, and per-segment sums of its chunks,
-//           every sum in a fixed order in float64.
+//           epilogue), then a deterministic segmented sum by token id: a
+//           stable counting sort of the token indices (per-block id
+//           histograms, per-id prefixes over the blocks, one scan over the
+//           vocabulary, and a bitonic sort of each block's (id, index) keys
+//           in LDS for the ranks within a block), per-chunk sums of at most
+//           64 rows of a segment, and per-segment sums of its chunks, every
+//           sum in a fixed order in float64.
 #include "sn_device.h"
 #include "sn_internal.h"
 
@@ -26,7 +28,8 @@ __device__ __forceinline__ int64_t ceil_div_dev(int64_t a, int64_t b) { return (
 constexpr int kChunk = 64;  // rows per chunk of a segment
 
 struct EmbedPlan {
-  int64_t kp = 0, maxseg = 0, maxchunk = 0;
+  int64_t kp = 0, maxseg = 0, maxchunk = 0, nblk = 0, ntile = 0;
+  size_t off_lz = 0, off_lch = 0, off_tiles = 0, off_count = 0;
   size_t off_c = 0, off_cnt = 0, off_cur = 0, off_order = 0, off_segid = 0, off_segoff = 0,
          off_segch = 0, off_cbeg = 0, off_cend = 0, off_meta = 0, off_part = 0, total = 0;
 };
@@ -46,12 +49,18 @@ EmbedPlan embed_plan(int64_t k, int dt, int64_t N, int64_t vocab, bool backward)
   }
   P.maxseg = N < vocab ? N : vocab;
   P.maxchunk = ceil_div(N, kChunk) + P.maxseg;
+  P.nblk = ceil_div(N, kSortThreads);
   auto ints = [&](size_t &o, int64_t n) {
     o = off;
     off = align256(off + static_cast<size_t>(n) * 4);
   };
-  ints(P.off_cnt, vocab);
-  ints(P.off_cur, vocab);
+  ints(P.off_cnt, P.nblk * vocab);  // per-block id counts, then their prefixes over blocks
+  ints(P.off_cur, vocab);           // per-id totals, then the ids' first slots
+  P.ntile = ceil_div(vocab, kSortThreads);
+  ints(P.off_count, vocab);         // per-id token counts
+  ints(P.off_lz, vocab);            // per id: segments and chunks before it in its tile
+  ints(P.off_lch, vocab);
+  ints(P.off_tiles, 6 * P.ntile);   // per tile: tokens, segments, chunks; then their offsets
   ints(P.off_order, N);
   ints(P.off_segid, P.maxseg);
   ints(P.off_segoff, P.maxseg + 1);
@@ -101,118 +110,207 @@ __device__ int block_excl_scan(int v, int *buf, int *total) {
   return incl - v;
 }
 
-// One workgroup: counting sort of the token indices by (clamped) id, stable,
-// and the segment and chunk tables.  meta[0] = segments, meta[1] = chunks.
-__global__ __launch_bounds__(kSortThreads) void sort_kernel(
-    const int32_t *__restrict__ tok, int64_t N, int64_t vocab, int32_t *err_flag,
-    int32_t *__restrict__ cnt, int32_t *__restrict__ cur, int32_t *__restrict__ order,
-    int32_t *__restrict__ seg_id, int32_t *__restrict__ seg_off, int32_t *__restrict__ seg_ch,
-    int32_t *__restrict__ cbeg, int32_t *__restrict__ cend, int32_t *__restrict__ meta) {
-  __shared__ int buf[kSortThreads];
-  __shared__ int sid[kSortThreads];
-  const int t = threadIdx.x;
-  const int nt = kSortThreads;
-  auto id_of = [&](int64_t i) {
-    int64_t v = tok[i];
-    if (v < 0 || v >= vocab) {
-      if (err_flag) atomicOr(err_flag, 1);
-      v = v < 0 ? 0 : vocab - 1;
-    }
-    return static_cast<int>(v);
-  };
-  // 1. histogram of the ids
-  for (int64_t v = t; v < vocab; v += nt) cnt[v] = 0;
-  __threadfence();
-  __syncthreads();
-  for (int64_t i = t; i < N; i += nt) atomicAdd(&cnt[id_of(i)], 1);
-  __threadfence();
-  __syncthreads();
-  // 2. offsets of the ids (thread t: ids [v0, v1)) and the segments (ids that occur)
-  const int64_t per = ceil_div_dev(vocab, nt);
-  const int64_t v0 = t * per < vocab ? t * per : vocab;
-  const int64_t v1 = v0 + per < vocab ? v0 + per : vocab;
-  int sum = 0, nz = 0;
-  for (int64_t v = v0; v < v1; ++v) {
-    sum += cnt[v];
-    nz += cnt[v] > 0;
+__device__ __forceinline__ int clamp_tok(const int32_t *tok, int64_t i, int64_t vocab,
+                                         int32_t *err_flag) {
+  int64_t v = tok[i];
+  if (v < 0 || v >= vocab) {
+    if (err_flag) atomicOr(err_flag, 1);
+    v = v < 0 ? 0 : vocab - 1;
   }
-  int total, nseg;
-  int run = block_excl_scan(sum, buf, &total);
-  int seg = block_excl_scan(nz, buf, &nseg);
-  for (int64_t v = v0; v < v1; ++v) {
-    const int c = cnt[v];
-    cur[v] = run;
-    if (c > 0) {
-      seg_id[seg] = static_cast<int>(v);
-      seg_off[seg] = run;
-      ++seg;
-    }
+  return static_cast<int>(v);
+}
+
+__global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// cnt[b][v] = number of tokens of block b (1024 tokens each) with id v
+__global__ __launch_bounds__(kSortThreads) void hist_kernel(const int32_t *__restrict__ tok,
+                                                            int64_t N, int64_t vocab,
+                                                            int32_t *err_flag,
+                                                            int32_t *__restrict__ cnt) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
+  if (i < N) atomicAdd(&cnt[static_cast<int64_t>(blockIdx.x) * vocab + clamp_tok(tok, i, vocab, err_flag)], 1);
+}
+
+// per id v: cnt[b][v] <- tokens of id v in the blocks before b; tot[v] <- all of them
+__global__ __launch_bounds__(256) void block_prefix_kernel(int32_t *__restrict__ cnt,
+                                                           int64_t nblk, int64_t vocab,
+                                                           int32_t *__restrict__ tot,
+                                                           int32_t *__restrict__ count) {
+  const int64_t v = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (v >= vocab) return;
+  int run = 0;
+  for (int64_t b = 0; b < nblk; ++b) {
+    const int c = cnt[b * vocab + v];
+    cnt[b * vocab + v] = run;
     run += c;
   }
-  if (t == 0) {
-    seg_off[nseg] = static_cast<int>(N);
-    meta[0] = nseg;
+  tot[v] = run;
+  count[v] = run;
+}
+
+// Scan over the vocabulary in three kernels.  Tile pass: per 1024-id tile,
+// exclusive prefixes within the tile of the ids' token counts, of the ids
+// that occur (segments) and of their chunks (at most kChunk rows each), and
+// the tile's three totals.
+__global__ __launch_bounds__(kSortThreads) void tile_scan_kernel(
+    int64_t vocab, int32_t *__restrict__ tot, int32_t *__restrict__ lz,
+    int32_t *__restrict__ lch, int32_t *__restrict__ tiles, int64_t ntile) {
+  __shared__ int buf[kSortThreads];
+  const int64_t v = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
+  const int c = v < vocab ? tot[v] : 0;
+  int sc, sz, sch;
+  const int ec = block_excl_scan(c, buf, &sc);
+  const int ez = block_excl_scan(c > 0, buf, &sz);
+  const int ech = block_excl_scan((c + kChunk - 1) / kChunk, buf, &sch);
+  if (v < vocab) {
+    tot[v] = ec;
+    lz[v] = ez;
+    lch[v] = ech;
   }
-  __threadfence();
+  if (threadIdx.x == 0) {
+    tiles[blockIdx.x] = sc;
+    tiles[ntile + blockIdx.x] = sz;
+    tiles[2 * ntile + blockIdx.x] = sch;
+  }
+}
+
+// One workgroup: exclusive prefixes of the tiles' totals (into tiles[3 ntile
+// ..]), the segment and chunk counts, and the end markers of both tables.
+__global__ __launch_bounds__(kSortThreads) void tiles_scan_kernel(
+    int64_t N, int32_t *__restrict__ tiles, int64_t ntile, int32_t *__restrict__ seg_off,
+    int32_t *__restrict__ seg_ch, int32_t *__restrict__ meta) {
+  __shared__ int buf[kSortThreads];
+  const int64_t per = ceil_div_dev(ntile, kSortThreads);
+  const int64_t t0 = threadIdx.x * per < ntile ? threadIdx.x * per : ntile;
+  const int64_t t1 = t0 + per < ntile ? t0 + per : ntile;
+  for (int a = 0; a < 3; ++a) {
+    int sum = 0;
+    for (int64_t i = t0; i < t1; ++i) sum += tiles[a * ntile + i];
+    int total;
+    int run = block_excl_scan(sum, buf, &total);
+    for (int64_t i = t0; i < t1; ++i) {
+      const int c = tiles[a * ntile + i];
+      tiles[(3 + a) * ntile + i] = run;
+      run += c;
+    }
+    if (threadIdx.x == 0 && a == 1) meta[0] = total;
+    if (threadIdx.x == 0 && a == 2) meta[1] = total;
+  }
   __syncthreads();
-  // 3. stable placement, 1024 tokens at a time: a token's slot is its id's
-  // cursor plus the number of earlier tokens of the chunk with the same id;
-  // the id's last token of the chunk advances the cursor
-  for (int64_t c0 = 0; c0 < N; c0 += nt) {
-    const int64_t i = c0 + t;
-    const int v = i < N ? id_of(i) : -1;
-    sid[t] = v;
-    __syncthreads();
-    int rank = 0;
-    bool last = true;
-    if (v >= 0) {
-      for (int j = 0; j < t; ++j) rank += sid[j] == v;
-      for (int j = t + 1; j < nt; ++j) last = last && sid[j] != v;
-      order[cur[v] + rank] = static_cast<int>(i);
+  if (threadIdx.x == 0) {
+    seg_off[meta[0]] = static_cast<int>(N);
+    seg_ch[meta[0]] = meta[1];
+  }
+}
+
+// Per id: its first slot, and for an id that occurs its segment entry and
+// chunk table entries.
+__global__ __launch_bounds__(kSortThreads) void tile_write_kernel(
+    int64_t vocab, const int32_t *__restrict__ cnt_last, int64_t nblk, int32_t *__restrict__ tot,
+    const int32_t *__restrict__ lz, const int32_t *__restrict__ lch,
+    const int32_t *__restrict__ tiles, int64_t ntile, int32_t *__restrict__ seg_id,
+    int32_t *__restrict__ seg_off, int32_t *__restrict__ seg_ch, int32_t *__restrict__ cbeg,
+    int32_t *__restrict__ cend, const int32_t *__restrict__ count) {
+  const int64_t tile = blockIdx.x;
+  const int64_t v = tile * kSortThreads + threadIdx.x;
+  if (v >= vocab) return;
+  const int first = tiles[3 * ntile + tile] + tot[v];
+  tot[v] = first;
+  const int c = count[v];
+  if (c == 0) return;
+  const int sgi = tiles[4 * ntile + tile] + lz[v];
+  int q = tiles[5 * ntile + tile] + lch[v];
+  seg_id[sgi] = static_cast<int>(v);
+  seg_off[sgi] = first;
+  seg_ch[sgi] = q;
+  for (int b = 0; b < c; b += kChunk, ++q) {
+    cbeg[q] = first + b;
+    cend[q] = first + (b + kChunk < c ? b + kChunk : c);
+  }
+  (void)cnt_last;
+  (void)nblk;
+}
+
+// Block b's tokens in sorted order: keys (id << 10 | local index) sorted in
+// LDS (bitonic), a token's rank among the block's tokens of its id is its
+// sorted position minus the first position of its id (a max scan of the run
+// heads), and its slot is first[id] + (id's tokens in earlier blocks) + rank.
+// Ids must be below 2^21.
+__global__ __launch_bounds__(kSortThreads) void place_kernel(
+    const int32_t *__restrict__ tok, int64_t N, int64_t vocab, const int32_t *__restrict__ cnt,
+    const int32_t *__restrict__ first, int32_t *__restrict__ order) {
+  __shared__ uint32_t key[kSortThreads];
+  __shared__ int hs[kSortThreads];
+  const int t = threadIdx.x;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortThreads;
+  const int64_t i = base + t;
+  key[t] = i < N ? (static_cast<uint32_t>(clamp_tok(tok, i, vocab, nullptr)) << 10) |
+                       static_cast<uint32_t>(t)
+                 : 0xFFFFFFFFu;
+  __syncthreads();
+  for (int kk = 2; kk <= kSortThreads; kk <<= 1) {
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      const int p = t ^ j;
+      if (p > t) {
+        const uint32_t a = key[t], b = key[p];
+        if ((a > b) == ((t & kk) == 0)) {
+          key[t] = b;
+          key[p] = a;
+        }
+      }
+      __syncthreads();
     }
+  }
+  const uint32_t me = key[t];
+  const bool head = t == 0 || (key[t - 1] >> 10) != (me >> 10);
+  hs[t] = head ? t : 0;
+  __syncthreads();
+  for (int off = 1; off < kSortThreads; off <<= 1) {  // inclusive max scan
+    const int o = t >= off ? hs[t - off] : 0;
     __syncthreads();
-    if (v >= 0 && last) cur[v] += rank + 1;
-    __threadfence();
+    hs[t] = hs[t] > o ? hs[t] : o;
     __syncthreads();
   }
-  // 4. chunks of at most kChunk rows per segment (thread t: segments [s0, s1))
-  const int64_t sper = ceil_div_dev(nseg, nt);
-  const int64_t s0 = t * sper < nseg ? t * sper : nseg;
-  const int64_t s1 = s0 + sper < nseg ? s0 + sper : nseg;
-  int nch = 0;
-  for (int64_t s = s0; s < s1; ++s) nch += (seg_off[s + 1] - seg_off[s] + kChunk - 1) / kChunk;
-  int nchunk;
-  int q = block_excl_scan(nch, buf, &nchunk);
-  for (int64_t s = s0; s < s1; ++s) {
-    seg_ch[s] = q;
-    for (int b = seg_off[s]; b < seg_off[s + 1]; b += kChunk) {
-      cbeg[q] = b;
-      cend[q] = b + kChunk < seg_off[s + 1] ? b + kChunk : seg_off[s + 1];
-      ++q;
-    }
-  }
-  if (t == 0) {
-    seg_ch[nseg] = nchunk;
-    meta[1] = nchunk;
+  if (me != 0xFFFFFFFFu) {
+    const int64_t id = me >> 10;
+    const int rank = t - hs[t];
+    const int64_t slot = first[id] + cnt[static_cast<int64_t>(blockIdx.x) * vocab + id] + rank;
+    order[slot] = static_cast<int32_t>(base + (me & 1023u));
   }
 }
 
 // One wave per chunk: part[q][j] = sum over the chunk's rows (ascending
-// token index) of c32[row][j], float64.
+// token index) of c32[row][j], float64.  Lane r copies row r of the chunk
+// into LDS (contiguous loads), then lane j adds column j down the rows.
 __global__ __launch_bounds__(256) void chunk_sum_kernel(const float *__restrict__ c32, int64_t kp,
                                                         const int32_t *__restrict__ order,
                                                         const int32_t *__restrict__ cbeg,
                                                         const int32_t *__restrict__ cend,
                                                         const int32_t *__restrict__ meta,
                                                         double *__restrict__ part) {
-  const int lane = threadIdx.x & 63;
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (q >= meta[1]) return;
-  const int b = cbeg[q], e = cend[q];
-  for (int64_t j = lane; j < kp; j += 64) {
-    double acc = 0.0;
-    for (int p = b; p < e; ++p) acc += static_cast<double>(c32[static_cast<int64_t>(order[p]) * kp + j]);
-    part[q * kp + j] = acc;
+  constexpr int JC = 64, LD = JC + 1;  // columns per pass, LDS row stride
+  __shared__ float rows[4][kChunk * LD];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + w;
+  const bool live = q < meta[1];
+  const int b = live ? cbeg[q] : 0, len = live ? cend[q] - b : 0;
+  float *rw = rows[w];
+  for (int64_t j0 = 0; j0 < kp; j0 += JC) {  // same trip count in every wave
+    const int64_t jn = kp - j0 < JC ? kp - j0 : JC;
+    if (lane < len) {
+      const float *src = c32 + static_cast<int64_t>(order[b + lane]) * kp + j0;
+      for (int64_t j = 0; j < jn; ++j) rw[lane * LD + j] = src[j];
+    }
+    __syncthreads();
+    if (live && lane < jn) {
+      double acc = 0.0;
+      for (int r = 0; r < len; ++r) acc += static_cast<double>(rw[r * LD + lane]);
+      part[q * kp + j0 + lane] = acc;
+    }
+    __syncthreads();
   }
 }
 
@@ -275,10 +373,22 @@ hipError_t launch_embed_backward(const PackLayout &L, const void *packed, const 
                      : launch_table_project_generic(L, packed, dX0, N, ldg, c32, P.kp, s);
   if (e != hipSuccess) return e;
   auto I = [&](size_t off) { return reinterpret_cast<int32_t *>(w + off); };
-  sort_kernel<<<dim3(1), kSortThreads, 0, s>>>(tok, N, vocab, err_flag, I(P.off_cnt), I(P.off_cur),
-                                                I(P.off_order), I(P.off_segid), I(P.off_segoff),
-                                                I(P.off_segch), I(P.off_cbeg), I(P.off_cend),
-                                                I(P.off_meta));
+  const int64_t nc = P.nblk * vocab;
+  zero_kernel<<<dim3(static_cast<unsigned>(ceil_div(nc, 256))), 256, 0, s>>>(I(P.off_cnt), nc);
+  hist_kernel<<<dim3(static_cast<unsigned>(P.nblk)), kSortThreads, 0, s>>>(tok, N, vocab,
+                                                                           err_flag, I(P.off_cnt));
+  block_prefix_kernel<<<dim3(static_cast<unsigned>(ceil_div(vocab, 256))), 256, 0, s>>>(
+      I(P.off_cnt), P.nblk, vocab, I(P.off_cur), I(P.off_count));
+  tile_scan_kernel<<<dim3(static_cast<unsigned>(P.ntile)), kSortThreads, 0, s>>>(
+      vocab, I(P.off_cur), I(P.off_lz), I(P.off_lch), I(P.off_tiles), P.ntile);
+  tiles_scan_kernel<<<dim3(1), kSortThreads, 0, s>>>(N, I(P.off_tiles), P.ntile, I(P.off_segoff),
+                                                      I(P.off_segch), I(P.off_meta));
+  tile_write_kernel<<<dim3(static_cast<unsigned>(P.ntile)), kSortThreads, 0, s>>>(
+      vocab, nullptr, 0, I(P.off_cur), I(P.off_lz), I(P.off_lch), I(P.off_tiles), P.ntile,
+      I(P.off_segid), I(P.off_segoff), I(P.off_segch), I(P.off_cbeg), I(P.off_cend),
+      I(P.off_count));
+  place_kernel<<<dim3(static_cast<unsigned>(P.nblk)), kSortThreads, 0, s>>>(
+      tok, N, vocab, I(P.off_cnt), I(P.off_cur), I(P.off_order));
   double *part = reinterpret_cast<double *>(w + P.off_part);
   chunk_sum_kernel<<<dim3(static_cast<unsigned>(ceil_div(P.maxchunk, 4))), 256, 0, s>>>(
       c32, P.kp, I(P.off_order), I(P.off_cbeg), I(P.off_cend), I(P.off_meta), part);
