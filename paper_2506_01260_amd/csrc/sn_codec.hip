@@ -95,11 +95,14 @@ struct CGeo {
   static constexpr int u_off = p_off + (HP ? p_rows<PM>() * kPieces : 0);
   static constexpr int u_frags = (kStageCols / 32) * KT;
   static constexpr int buf_units = u_off + u_frags * 64;
+  // with both tables, the positional rows go with the U fragments so the
+  // three producers issue about as many copies each
+  static constexpr bool p_with_u = HE && HP;
   // copy instructions per stage of each producer: X; gathered rows; U
   static constexpr int dma_a = kTokens / kRowsPerCopy;
-  static constexpr int dma_b =
-      (HE ? kTokens / kRowsPerCopy : 0) + (HP ? p_rows<PM>() / kRowsPerCopy : 0);
-  static constexpr int dma_c = u_frags;
+  static constexpr int dma_p = HP ? p_rows<PM>() / kRowsPerCopy : 0;
+  static constexpr int dma_b = (HE ? kTokens / kRowsPerCopy : 0) + (p_with_u ? 0 : dma_p);
+  static constexpr int dma_c = u_frags + (p_with_u ? dma_p : 0);
   static constexpr int dmax = dma_a > dma_b ? (dma_a > dma_c ? dma_a : dma_c)
                                             : (dma_b > dma_c ? dma_b : dma_c);
   // as many stages as LDS holds (at most kMaxStages), with (nb - 2) stages of
@@ -191,7 +194,10 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
   const int64_t T0 = static_cast<int64_t>(blockIdx.x) * kW;
 
   if (wave >= kW) {  // ------------------------------------------------ producers
-    const int role = wave - kW;  // 0: X rows, 1: T_fixed and P rows, 2: U fragments
+    // 0: X rows; 1: T_fixed rows (and P rows with no T_fixed); 2: U fragments
+    // (and P rows with both tables)
+    const int role = wave - kW;
+    const int prole = G::p_with_u ? 2 : 1;  // the producer that copies P rows
     const int q = lane / kPieces, m = lane % kPieces;
     RowSet<kTokens> rx, re;
     RowSet<p_rows<PM>()> rp;
@@ -205,18 +211,24 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
 #pragma unroll
       for (int i = 0; i < kTokens / kRowsPerCopy; ++i)
         rx.ptr[i] = X + token_of(kRowsPerCopy * i + q) * ldx;
-    } else if (role == 1) {
+    }
+    if (role == 1 && HE) {
 #pragma unroll
       for (int i = 0; i < kTokens / kRowsPerCopy; ++i) {
         const int64_t t = token_of(kRowsPerCopy * i + q);
-        if (HE) re.ptr[i] = row_ptr(ids.E, ids.lde, clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1));
-        if (HP && !PM) {
+        re.ptr[i] = row_ptr(ids.E, ids.lde, clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1));
+      }
+    }
+    if (role == prole && HP) {
+      if (!PM) {
+#pragma unroll
+        for (int i = 0; i < kTokens / kRowsPerCopy; ++i) {
+          const int64_t t = token_of(kRowsPerCopy * i + q);
           int64_t ps = ids.pos ? static_cast<int64_t>(ids.pos[t]) : t % ids.seq_len;
           ps = clamp_id(ps, ids.n_pos, ids.err_flag, 2);
           rp.ptr[i] = row_ptr(ids.P, ids.ldp, ps);
         }
-      }
-      if (HP && PM) {
+      } else {
         // positional row r = w * pg + rho of the workgroup (rows past 4 pg
         // repeat the last one so the copy count stays fixed)
         const int pg = 16 / tm.bp;
@@ -240,10 +252,11 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
         dma_rows<kTokens, EPI != kEpiGrass>(rx, col, b + G::x_off, q, m);
       } else if (role == 1) {
         if (HE) dma_rows(re, col, b + G::e_off, q, m);
-        if (HP) dma_rows(rp, col, b + G::p_off, q, m);
+        if (HP && !G::p_with_u) dma_rows(rp, col, b + G::p_off, q, m);
       } else {
         dma_frags(kfrag + static_cast<int64_t>(st) * G::u_frags * 512, G::u_frags, b + G::u_off,
                   lane);
+        if (HP && G::p_with_u) dma_rows(rp, col, b + G::p_off, q, m);
       }
     };
     for (int s = 0; s < NB - 1; ++s)
