@@ -7,7 +7,7 @@ One step = the whole hot path for one batch at d=4096, k=40, N=32768 tokens
   decompress    X' = C U^T + P[pos] + E[tok]
   grad compress Cg = G U
   grad decomp.  G' = Cg U^T
-  projection    Wo (4096 x 4096) and W2 (4096 x 14336) <- U (U^T W), in place
+  projection    Wo (4096 x 4096) and W2 (4096 x 14336) <- U (U^T W), in place, one call
 
 Inputs are resident in HBM before timing; X, G, the outputs and the weights
 rotate over several buffer sets so no step finds its data in the 256 MB
@@ -436,12 +436,14 @@ def other_configs(sn, torch, steps: int) -> dict:
     basis = sn.sn_basis_pack(U)
     mats = [synth.device_weight(3, 2 * layer + i, r, c)
             for layer in range(cfg.layers) for i, (r, c) in enumerate(cfg.weights)]
-    ws = torch.empty(max(sn.sn_project_weights_workspace_bytes(cfg.d, cfg.k, sn.SN_BF16, c)
-                         for _, c in cfg.weights), dtype=torch.uint8, device="cuda")
+    group = 16  # matrices per call: 8 layers of (Wo, W2)
+    ws = torch.empty(sn.sn_project_weights_multi_workspace_bytes(
+        cfg.d, cfg.k, sn.SN_BF16, [Wm.shape[1] for Wm in mats[:group]]),
+        dtype=torch.uint8, device="cuda")
 
     def sweep():
-        for Wm in mats:
-            sn.sn_project_weights(basis, Wm, workspace=ws)
+        for g0 in range(0, len(mats), group):
+            sn.sn_project_weights_multi(basis, mats[g0:g0 + group], workspace=ws)
 
     sweep()
     torch.cuda.synchronize()
@@ -678,8 +680,8 @@ def main():
         base = to_dev(wb)
         weights.append([base.clone() for _ in range(R)])
         del base
-    ws_bytes = max(sn.sn_project_weights_workspace_bytes(d, k, sn.SN_BF16, c)
-                   for _, c in cfg.weights)
+    ws_bytes = sn.sn_project_weights_multi_workspace_bytes(d, k, sn.SN_BF16,
+                                                          [c for _, c in cfg.weights])
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
 
     # algorithmic bytes per op: inputs and outputs, each unique gathered row once, U once
@@ -695,8 +697,8 @@ def main():
         "grad_compress": xb + cb + ub,
         "grad_decompress": cb + xb + ub,
     }
-    for i, (rows, cols) in enumerate(cfg.weights):
-        op_bytes[f"project_W{i}"] = 2 * rows * cols * es
+    # the layer's projection matrices (Wo and W2), confined in one call
+    op_bytes["project_weights"] = sum(2 * rows * cols * es for rows, cols in cfg.weights)
     # the projected-table compress reads k-wide fp32 projected rows instead of d-wide ones
     alt_bytes = {"compress_projected": xb + cb + ub + (uniq_tok + min(cfg.seq, N)) * kp * 4,
                  "embed_project": (cfg.vocab + cfg.seq) * d * es + (cfg.vocab + cfg.seq) * kp * 4
@@ -718,9 +720,10 @@ def main():
             sn.sn_compress_projected(basis, Xs[j], proj, tok=tok, seq_len=cfg.seq, out=Cps[j])
         elif name == "embed_project":
             sn.sn_embed_project(basis, E=E, P=P)
+        elif name == "project_weights":
+            sn.sn_project_weights_multi(basis, [wl[j] for wl in weights], workspace=ws)
         else:
-            wi = int(name[len("project_W"):])
-            sn.sn_project_weights(basis, weights[wi][j], workspace=ws)
+            raise ValueError(name)
 
     names = list(op_bytes)
     stream = torch.cuda.current_stream()

@@ -213,6 +213,23 @@ int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt,
                            void *W, int64_t m, int64_t ldw,
                            void *workspace, size_t workspace_bytes, sn_stream stream);
 
+/* Several weights confined in one call (the optimizer step's sweep over a
+ * layer's or a model's projection matrices, Sec. 5): W[i] (d x m[i], row
+ * stride ldw[i]) <- U (U^T W[i]) for i < count.  When every width is a
+ * multiple of 256 (bf16, k <= 64) the matrices are processed side by side as
+ * one d x (sum of m[i]) matrix by one set of launches, which keeps the chip
+ * busy where a single small matrix cannot; otherwise they are projected one
+ * after another.  W, m and ldw are HOST arrays of count entries; the matrices
+ * are device memory and may not overlap each other, the basis or the
+ * workspace.  count <= SN_PROJECT_MAX_MATRICES.  Errors as sn_project_weights. */
+#define SN_PROJECT_MAX_MATRICES 16
+size_t sn_project_weights_multi_workspace_bytes(int64_t d, int64_t k, int32_t dt, int32_t count,
+                                                const int64_t *m);
+int32_t sn_project_weights_multi(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                 int32_t count, void *const *W, const int64_t *m,
+                                 const int64_t *ldw, void *workspace, size_t workspace_bytes,
+                                 sn_stream stream);
+
 /* ------------------------------------------------------------------------ */
 /* Subspace update (Sec. 4.5; cost analysis of Sec. 6).                        */
 /*                                                                            */

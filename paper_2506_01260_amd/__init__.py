@@ -60,6 +60,8 @@ _SIGNATURES = {
                                      _I64, _I64, _P, _I64, _P, _P]),
     "sn_project_weights_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
     "sn_project_weights": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _SZ, _P]),
+    "sn_project_weights_multi_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I32, _P]),
+    "sn_project_weights_multi": (_I32, [_P, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _SZ, _P]),
     "sn_grassmann_state_bytes": (_SZ, [_I64, _I64]),
     "sn_grassmann_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
     "sn_grassmann_reset": (_I32, [_P, _I64, _I64, _P]),
@@ -339,6 +341,40 @@ def sn_project_weights(basis: Basis, W: torch.Tensor, workspace=None, stream=Non
     _check(lib().sn_project_weights(basis.ptr, d, basis.k, basis.dt, wp, m, ldw,
                                     workspace.data_ptr(), workspace.numel(), _stream(stream)))
     return W
+
+
+def _i64_array(vals):
+    arr = (ctypes.c_int64 * max(1, len(vals)))(*vals)
+    return arr
+
+
+def sn_project_weights_multi_workspace_bytes(d: int, k: int, dt: int, widths) -> int:
+    m = _i64_array(widths)
+    return lib().sn_project_weights_multi_workspace_bytes(d, k, dt, len(widths), m)
+
+
+def sn_project_weights_multi(basis: Basis, Ws, workspace=None, stream=None):
+    """W <- U (U^T W) in place for every matrix of the list Ws (each d x m_i),
+    in one set of launches when the widths allow; returns Ws."""
+    ptrs, widths, lds = [], [], []
+    for i, W in enumerate(Ws):
+        wp, d, m, ldw = _mat(W, f"W[{i}]")
+        if d != basis.d:
+            raise SnError(2, f"W[{i}] has {d} rows, basis has d = {basis.d}")
+        _same_dtype(basis, (f"W[{i}]", W))
+        ptrs.append(wp)
+        widths.append(m)
+        lds.append(ldw)
+    need = sn_project_weights_multi_workspace_bytes(basis.d, basis.k, basis.dt, widths)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=Ws[0].device)
+    if workspace.numel() < need or not workspace.is_cuda:
+        raise SnError(9, f"workspace needs {need} device bytes")
+    parr = (ctypes.c_void_p * max(1, len(ptrs)))(*ptrs)
+    _check(lib().sn_project_weights_multi(basis.ptr, basis.d, basis.k, basis.dt, len(Ws), parr,
+                                          _i64_array(widths), _i64_array(lds),
+                                          workspace.data_ptr(), workspace.numel(), _stream(stream)))
+    return Ws
 
 
 class GrassmannState:

@@ -615,6 +615,105 @@ int32_t sn_adamw_step(void *W, int64_t ldw, const void *G, int64_t ldg, int32_t 
                     "sn_adamw_step launch");
 }
 
+namespace {
+
+// The segmented (one set of launches) form applies when every matrix meets
+// the MFMA path's conditions with a width that is a multiple of 256.
+bool multi_segmented(const sn::PackLayout &L, int32_t count, void *const *W, const int64_t *m,
+                     const int64_t *ldw) {
+  if (!L.mfma || L.ks2 == 0 || count < 1 || count > sn::kMaxSeg) return false;
+  for (int32_t i = 0; i < count; ++i)
+    if (m[i] % 256 != 0 || !sn::project_mfma_ok(L, W[i], m[i], ldw[i])) return false;
+  return true;
+}
+
+}  // namespace
+
+size_t sn_project_weights_multi_workspace_bytes(int64_t d, int64_t k, int32_t dt, int32_t count,
+                                                const int64_t *m) {
+  if (!dtype_ok(dt) || d < 1 || d >= kMaxDim || k < 1 || k > d || k > SN_MAX_K || count < 0 ||
+      count > SN_PROJECT_MAX_MATRICES || (count > 0 && !m))
+    return 0;
+  size_t best = 0;
+  int64_t total = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    if (m[i] < 0 || m[i] >= kMaxDim) return 0;
+    const size_t one = sn_project_weights_workspace_bytes(d, k, dt, m[i]);
+    best = one > best ? one : best;
+    total += m[i];
+  }
+  if (total >= kMaxDim) return 0;
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  if (L.mfma && total > 0) {
+    const size_t seg = sn::align256(sn::project_workspace_mfma(d, k, total));
+    best = seg > best ? seg : best;
+  }
+  return best;
+}
+
+int32_t sn_project_weights_multi(const void *basis, int64_t d, int64_t k, int32_t dt, int32_t count,
+                                 void *const *W, const int64_t *m, const int64_t *ldw,
+                                 void *workspace, size_t workspace_bytes, sn_stream stream) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (count < 0 || count > SN_PROJECT_MAX_MATRICES)
+    return fail(SN_ERR_SHAPE, "count must lie in [0, %d]", SN_PROJECT_MAX_MATRICES);
+  if (count == 0) return ok();
+  if (!W || !m || !ldw) return fail(SN_ERR_NULL, "W, m and ldw arrays are required");
+  int64_t total = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    if (m[i] < 0 || m[i] >= kMaxDim) return fail(SN_ERR_SHAPE, "m[%d] out of range", i);
+    if (ldw[i] < m[i] || ldw[i] >= kMaxDim) return fail(SN_ERR_SHAPE, "ldw[%d] must be >= m[%d]", i, i);
+    if (m[i] > 0 && !W[i]) return fail(SN_ERR_NULL, "W[%d] is NULL", i);
+    if (m[i] > 0 && !elem_aligned(W[i], dt)) return fail(SN_ERR_ALIGN, "W[%d] misaligned", i);
+    total += m[i];
+  }
+  if (total >= kMaxDim) return fail(SN_ERR_SHAPE, "total width out of range");
+  if (total == 0) return ok();
+  if (!workspace) return fail(SN_ERR_NULL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    return fail(SN_ERR_ALIGN, "workspace must be 256-byte aligned");
+  const size_t need = sn_project_weights_multi_workspace_bytes(d, k, dt, count, m);
+  if (workspace_bytes < need)
+    return fail(SN_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  const sn::PackLayout L = sn::pack_layout(d, k, dt);
+  const size_t es = elem_size(dt);
+  const Span ws = bytes_span(workspace, need), b = bytes_span(basis, L.total);
+  if (overlap(ws, b)) return fail(SN_ERR_ALIAS, "workspace overlaps the basis");
+  for (int32_t i = 0; i < count; ++i) {
+    const Span wi = span(W[i], d, m[i], ldw[i], es);
+    if (overlap(wi, ws) || overlap(wi, b))
+      return fail(SN_ERR_ALIAS, "W[%d] overlaps the workspace or the basis", i);
+    for (int32_t j = 0; j < i; ++j)
+      if (overlap(wi, span(W[j], d, m[j], ldw[j], es)))
+        return fail(SN_ERR_ALIAS, "W[%d] overlaps W[%d]", i, j);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (multi_segmented(L, count, W, m, ldw)) {
+    sn::ColSegs cs;
+    cs.n = 0;
+    int64_t c0 = 0;
+    for (int32_t i = 0; i < count; ++i) {
+      if (m[i] == 0) continue;
+      cs.c0[cs.n] = c0;
+      cs.base[cs.n] = W[i];
+      cs.ld[cs.n] = ldw[i];
+      ++cs.n;
+      c0 += m[i];
+    }
+    cs.c0[cs.n] = c0;
+    return hip_status(sn::launch_project_mfma_segs(L, basis, cs, workspace, s),
+                      "sn_project_weights_multi launch");
+  }
+  for (int32_t i = 0; i < count; ++i) {  // one after another, sharing the workspace
+    if (m[i] == 0) continue;
+    if ((st = sn_project_weights(basis, d, k, dt, W[i], m[i], ldw[i], workspace, workspace_bytes,
+                                 stream)))
+      return st;
+  }
+  return ok();
+}
+
 const char *sn_status_string(int32_t status) {
   switch (status) {
     case SN_OK: return "SN_OK";

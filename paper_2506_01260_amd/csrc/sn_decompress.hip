@@ -137,7 +137,7 @@ struct DSmemPlain {
 template <int KS, bool HE, bool HP, int CM>
 __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     const bf16_t *__restrict__ rfrag, int64_t k, const bf16_t *__restrict__ C, int64_t ldc,
-    DTiling tm, IdArgs ids, bf16_t *__restrict__ X, int64_t ldx, int ncb, int ntiles,
+    DTiling tm, IdArgs ids, ColSegs xs, int ncb, int ntiles,
     int tiles_per_wg) {
   constexpr int FR = 2 * KS;  // fragments per row group
   __shared__ u32x4 us[kPG * FR * 64];
@@ -202,6 +202,10 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   if (nt == 0) return;
 
   const int64_t col_r = static_cast<int64_t>(cb) * kDCols + 8 * m;  // row-layout column
+  // the column segment of X that holds this block (blocks never straddle two)
+  int sg = 0;
+  while (sg + 1 < xs.n && static_cast<int64_t>(cb) * kDCols >= xs.c0[sg + 1]) ++sg;
+  const int64_t ldx = xs.ld[sg];
   f32x4 *otw = sm.ot[wave];
   int bad = 0;
 
@@ -222,7 +226,7 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   };
   const bf16_t *Eb = static_cast<const bf16_t *>(ids.E) + col_r;
   const bf16_t *Pb = static_cast<const bf16_t *>(ids.P) + col_r;
-  bf16_t *Xb = X + col_r;
+  bf16_t *Xb = static_cast<bf16_t *>(xs.base[sg]) + (col_r - xs.c0[sg]);
   // The P values are reloaded only when the tile's positions change: in
   // position-major order a wave's run of tiles holds `batch` tiles with the
   // same 16 positions in a row, and slot c of the ring keeps chunk c.
@@ -333,7 +337,7 @@ int64_t resident_slots(K kernel) {
 
 template <int KS, bool HE, bool HP, int CM>
 void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
-                const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+                const DTiling &tm, const IdArgs &ids, const ColSegs &X, hipStream_t s) {
   const int ncb = static_cast<int>(L.d / kDCols);
   const int64_t ntiles = ceil_div(tm.N, 16);
   // one round of resident workgroups over the whole grid, whole waves of tiles
@@ -345,33 +349,33 @@ void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ld
   const int64_t tgroups = ceil_div(ntiles, per);
   dim3 grid(static_cast<unsigned>(tgroups * ncb));
   decompress_cb_kernel<KS, HE, HP, CM><<<grid, kDThreads, 0, s>>>(
-      rf, L.k, static_cast<const bf16_t *>(C), ldc, tm, ids, static_cast<bf16_t *>(X), ldx, ncb,
+      rf, L.k, static_cast<const bf16_t *>(C), ldc, tm, ids, X, ncb,
       static_cast<int>(ntiles), static_cast<int>(per));
 }
 
 template <int KS, int CM>
 void launch_dcb_t(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
-                  const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+                  const DTiling &tm, const IdArgs &ids, const ColSegs &X, hipStream_t s) {
   const bool he = ids.E != nullptr, hp = ids.P != nullptr;
   if (he && hp)
-    launch_dcb<KS, true, true, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb<KS, true, true, CM>(rf, L, C, ldc, tm, ids, X, s);
   else if (he)
-    launch_dcb<KS, true, false, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb<KS, true, false, CM>(rf, L, C, ldc, tm, ids, X, s);
   else if (hp)
-    launch_dcb<KS, false, true, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb<KS, false, true, CM>(rf, L, C, ldc, tm, ids, X, s);
   else
-    launch_dcb<KS, false, false, CM>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb<KS, false, false, CM>(rf, L, C, ldc, tm, ids, X, s);
 }
 
 template <int KS>
 void launch_dcb_ks(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc, int cmode,
-                   const DTiling &tm, const IdArgs &ids, void *X, int64_t ldx, hipStream_t s) {
+                   const DTiling &tm, const IdArgs &ids, const ColSegs &X, hipStream_t s) {
   if (cmode == 0)
-    launch_dcb_t<KS, 0>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb_t<KS, 0>(rf, L, C, ldc, tm, ids, X, s);
   else if (cmode == 1)
-    launch_dcb_t<KS, 1>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb_t<KS, 1>(rf, L, C, ldc, tm, ids, X, s);
   else
-    launch_dcb_t<KS, 2>(rf, L, C, ldc, tm, ids, X, ldx, s);
+    launch_dcb_t<KS, 2>(rf, L, C, ldc, tm, ids, X, s);
 }
 
 bool table_ok(const void *T, int64_t ld) { return !T || (aligned16(T) && ld % 8 == 0); }
@@ -386,6 +390,12 @@ bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs 
 hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const void *C,
                                   int64_t N, int64_t ldc, const IdArgs &ids, void *X,
                                   int64_t ldx, hipStream_t s) {
+  return launch_decompress_mfma_segs(L, packed, C, N, ldc, ids, one_seg(X, L.d, ldx), s);
+}
+
+hipError_t launch_decompress_mfma_segs(const PackLayout &L, const void *packed, const void *C,
+                                       int64_t N, int64_t ldc, const IdArgs &ids,
+                                       const ColSegs &X, hipStream_t s) {
   const bf16_t *rf =
       reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_rfrag);
   // how the coefficient rows may be read: 16-byte chunks, 4-byte pairs, or bf16 by bf16
@@ -400,10 +410,10 @@ hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const
     tm.batch = static_cast<int>(N / ids.seq_len);
   }
   switch (L.ks) {
-    case 1: launch_dcb_ks<1>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
-    case 2: launch_dcb_ks<2>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
-    case 3: launch_dcb_ks<3>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
-    case 4: launch_dcb_ks<4>(rf, L, C, ldc, cmode, tm, ids, X, ldx, s); break;
+    case 1: launch_dcb_ks<1>(rf, L, C, ldc, cmode, tm, ids, X, s); break;
+    case 2: launch_dcb_ks<2>(rf, L, C, ldc, cmode, tm, ids, X, s); break;
+    case 3: launch_dcb_ks<3>(rf, L, C, ldc, cmode, tm, ids, X, s); break;
+    case 4: launch_dcb_ks<4>(rf, L, C, ldc, cmode, tm, ids, X, s); break;
     default: return hipErrorNotSupported;
   }
   return hipGetLastError();

@@ -46,6 +46,27 @@ struct PackLayout {
 
 PackLayout pack_layout(int64_t d, int64_t k, int dt);
 
+// A matrix given as column segments side by side, each with its own base
+// pointer and row stride: segment s holds global columns [c0[s], c0[s+1]).
+// The decompress and projection kernels read and write it as one matrix, so
+// several weights of the same d are projected by one set of launches.
+constexpr int kMaxSeg = 16;  // SN_PROJECT_MAX_MATRICES
+struct ColSegs {
+  int n = 1;
+  int64_t c0[kMaxSeg + 1] = {};
+  void *base[kMaxSeg] = {};
+  int64_t ld[kMaxSeg] = {};
+};
+inline ColSegs one_seg(const void *p, int64_t cols, int64_t ld) {
+  ColSegs c;
+  c.n = 1;
+  c.c0[0] = 0;
+  c.c0[1] = cols;
+  c.base[0] = const_cast<void *>(p);
+  c.ld[0] = ld;
+  return c;
+}
+
 // ---- launchers (arguments already validated; N > 0) ----------------------
 struct IdArgs {
   const int32_t *tok;
@@ -81,6 +102,10 @@ bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs 
 hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const void *C,
                                   int64_t N, int64_t ldc, const IdArgs &ids, void *X,
                                   int64_t ldx, hipStream_t s);
+// the same with X given as column segments (each width a multiple of 256)
+hipError_t launch_decompress_mfma_segs(const PackLayout &L, const void *packed, const void *C,
+                                       int64_t N, int64_t ldc, const IdArgs &ids,
+                                       const ColSegs &X, hipStream_t s);
 
 // Projected tables: T_fixed U (vocab rows) then P U (n_pos rows), fp32, row
 // stride kp = 16 * ceil(k / 16) (columns k..kp-1 are zero), the P U section at
@@ -171,6 +196,10 @@ hipError_t launch_grass_step(const PackLayout &L, const void *packed, const void
                              double eta, void *Unew, int64_t ldu, int out_dt, void *ws,
                              int32_t *err_flag, hipStream_t s);
 bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw);
+// W <- U (U^T W) for the matrix of column segments W (every width a multiple
+// of 256 when there is more than one segment); workspace for the total width
+hipError_t launch_project_mfma_segs(const PackLayout &L, const void *packed, const ColSegs &W,
+                                   void *ws, hipStream_t s);
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *W, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s);
 

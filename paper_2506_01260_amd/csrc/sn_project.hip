@@ -63,6 +63,9 @@ ProjPlan proj_plan(int64_t k, int kt, int ks, int64_t m, int64_t d, int64_t slot
   const int64_t slabs = ceil_div(m, 16 * (kt <= 4 ? 8 : 4));  // pass-1 workgroups per split
   int64_t max_ds = d / 128;  // >= 32 rows per wave
   if (max_ds > 8) max_ds = 8;
+  // wide matrices (several weights side by side) fill the chip with few splits
+  const int64_t by_cols = ceil_div(1024, slabs);
+  if (max_ds > by_cols) max_ds = by_cols;
   if (max_ds < 1) max_ds = 1;
   int64_t best = max_ds, best_cost = -1;
   if (slots > 0) {
@@ -104,9 +107,8 @@ template <> struct P1Vec<4> { typedef u32x2 T; };
 // the split size (the subspace update's contraction over tokens).
 template <int KT, bool CLAMP = false, int CW = p1_cw<KT>()>
 __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
-    const bf16_t *__restrict__ kfrag, int64_t d, const bf16_t *__restrict__ W, int64_t m,
-    int64_t ldw, int64_t rows_per_split, int64_t m_pad, float *__restrict__ Tp,
-    int64_t nrows = 0) {
+    const bf16_t *__restrict__ kfrag, int64_t d, ColSegs ws, int64_t rows_per_split,
+    int64_t m_pad, float *__restrict__ Tp, int64_t nrows = 0) {
   constexpr int W32 = CW / 2;  // 32-bit words per lane and row
   typedef typename P1Vec<CW>::T vec;
   __shared__ f32x4 red[KT][CW][64];
@@ -117,8 +119,14 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
   // CLAMP (the token contraction) takes the splits last-first: the rows the
   // preceding pass read last are the likeliest still to be cached
   const int split = CLAMP ? static_cast<int>(gridDim.y - 1 - blockIdx.y) : blockIdx.y;
-  const int64_t col = cb + CW * n;
-  const bool cvalid = col < m;  // m % 8 == 0: all CW columns are valid
+  // the column segment holding this block (blocks never straddle two)
+  int sg = 0;
+  while (sg + 1 < ws.n && cb >= ws.c0[sg + 1]) ++sg;
+  const bf16_t *__restrict__ W = static_cast<const bf16_t *>(ws.base[sg]);
+  const int64_t ldw = ws.ld[sg];
+  const int64_t col = cb + CW * n;           // global column (T's layout)
+  const int64_t lcol = col - ws.c0[sg];      // column within the segment
+  const bool cvalid = col < ws.c0[sg + 1];   // widths % 8 == 0: all CW columns are valid
 
   const int steps = static_cast<int>(rows_per_split / 32);
   const int sb = static_cast<int>(split * (rows_per_split / 32));
@@ -135,7 +143,7 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
 
   // Lanes past column m read column 0 instead (any finite values): every
   // load is unconditional and their columns are never stored.
-  const bf16_t *wcol = W + (cvalid ? col : 0);
+  const bf16_t *wcol = W + (cvalid ? lcol : 0);
   const bf16_t *ufrag = kfrag + lane * 8;
   // rows 32 s + 8 g + e of the lane's CW columns, and the step's U fragments
   auto load = [&](int s, vec (&v)[8], u32x4 (&a)[KT]) {
@@ -364,11 +372,10 @@ __global__ __launch_bounds__(kBlock) void project_pass3_kernel(
 }
 
 template <int KT>
-void launch_p1(const ProjPlan &P, const bf16_t *kf, int64_t d, const bf16_t *W, int64_t m,
-               int64_t ldw, float *Tp, hipStream_t s) {
+void launch_p1(const ProjPlan &P, const bf16_t *kf, int64_t d, const ColSegs &W, int64_t m,
+               float *Tp, hipStream_t s) {
   dim3 grid(static_cast<unsigned>(ceil_div(m, 16 * p1_cw<KT>())), static_cast<unsigned>(P.dsplit));
-  project_pass1_kernel<KT><<<grid, kBlock, 0, s>>>(kf, d, W, m, ldw, P.rows_per_split, P.m_pad,
-                                                   Tp);
+  project_pass1_kernel<KT><<<grid, kBlock, 0, s>>>(kf, d, W, P.rows_per_split, P.m_pad, Tp);
 }
 
 template <int KS>
@@ -427,8 +434,8 @@ void launch_p1_tokens(const bf16_t *frag, int64_t npad, const bf16_t *G, int64_t
                       int64_t d, int64_t rows, int ds, int64_t m_pad, float *Tp, hipStream_t s) {
   constexpr int CW = tok_cw<KT>();
   dim3 grid(static_cast<unsigned>(ceil_div(d, 16 * CW)), static_cast<unsigned>(ds));
-  project_pass1_kernel<KT, true, CW><<<grid, kBlock, 0, s>>>(frag, npad, G, d, ldg, rows, m_pad,
-                                                              Tp, N);
+  project_pass1_kernel<KT, true, CW><<<grid, kBlock, 0, s>>>(frag, npad, one_seg(G, d, ldg),
+                                                              rows, m_pad, Tp, N);
 }
 
 hipError_t launch_grass_tokens_mfma(const void *frag, int ktb, int64_t npad, const void *G,
@@ -461,6 +468,12 @@ bool project_mfma_ok(const PackLayout &L, const void *W, int64_t m, int64_t ldw)
 
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s) {
+  return launch_project_mfma_segs(L, packed, one_seg(Wv, m, ldw), ws, s);
+}
+
+hipError_t launch_project_mfma_segs(const PackLayout &L, const void *packed, const ColSegs &W,
+                                   void *ws, hipStream_t s) {
+  const int64_t m = W.c0[W.n];
   const ProjPlan P = proj_plan(L.k, L.kt, L.ks, m, L.d, pass1_slots(L.kt));
   const char *base = static_cast<const char *>(packed);
   const bf16_t *kf = reinterpret_cast<const bf16_t *>(base + L.off_kfrag);
@@ -469,16 +482,15 @@ hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv
   float *Tp = reinterpret_cast<float *>(w + P.off_tp);
   bf16_t *Th = reinterpret_cast<bf16_t *>(w + P.off_th);
   bf16_t *Tl = reinterpret_cast<bf16_t *>(w + P.off_tl);
-  bf16_t *W = static_cast<bf16_t *>(Wv);
   switch (L.kt) {
-    case 1: launch_p1<1>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 2: launch_p1<2>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 3: launch_p1<3>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 4: launch_p1<4>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 5: launch_p1<5>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 6: launch_p1<6>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 7: launch_p1<7>(P, kf, L.d, W, m, ldw, Tp, s); break;
-    case 8: launch_p1<8>(P, kf, L.d, W, m, ldw, Tp, s); break;
+    case 1: launch_p1<1>(P, kf, L.d, W, m, Tp, s); break;
+    case 2: launch_p1<2>(P, kf, L.d, W, m, Tp, s); break;
+    case 3: launch_p1<3>(P, kf, L.d, W, m, Tp, s); break;
+    case 4: launch_p1<4>(P, kf, L.d, W, m, Tp, s); break;
+    case 5: launch_p1<5>(P, kf, L.d, W, m, Tp, s); break;
+    case 6: launch_p1<6>(P, kf, L.d, W, m, Tp, s); break;
+    case 7: launch_p1<7>(P, kf, L.d, W, m, Tp, s); break;
+    case 8: launch_p1<8>(P, kf, L.d, W, m, Tp, s); break;
     default: return hipErrorNotSupported;
   }
   if (L.ks2 > 0 && m % 256 == 0) {
@@ -497,17 +509,20 @@ hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *Wv
     V.ks = P.ks2;
     V.off_rfrag = P.off_tr;
     IdArgs none{};
-    const hipError_t e = launch_decompress_mfma(V, ws, uu, L.d, 32 * P.ks2, none, W, ldw, s);
+    const hipError_t e = launch_decompress_mfma_segs(V, ws, uu, L.d, 32 * P.ks2, none, W, s);
     return e != hipSuccess ? e : hipGetLastError();
   }
+  if (W.n != 1) return hipErrorNotSupported;  // the segmented form needs widths % 256 == 0
   const int64_t n2 = P.m_pad * P.kp32;
   project_pass2_kernel<<<dim3(static_cast<unsigned>(ceil_div(n2, 256))), 256, 0, s>>>(
       Tp, P.dsplit, m, P.m_pad, P.kp, P.kp32, Th, Tl);
+  bf16_t *Wp = static_cast<bf16_t *>(W.base[0]);
+  const int64_t ldw = W.ld[0];
   switch (L.ks) {
-    case 1: launch_p3<1>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
-    case 2: launch_p3<2>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
-    case 3: launch_p3<3>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
-    case 4: launch_p3<4>(P, rf, L.d, Th, Tl, W, m, ldw, s); break;
+    case 1: launch_p3<1>(P, rf, L.d, Th, Tl, Wp, m, ldw, s); break;
+    case 2: launch_p3<2>(P, rf, L.d, Th, Tl, Wp, m, ldw, s); break;
+    case 3: launch_p3<3>(P, rf, L.d, Th, Tl, Wp, m, ldw, s); break;
+    case 4: launch_p3<4>(P, rf, L.d, Th, Tl, Wp, m, ldw, s); break;
     default: return hipErrorNotSupported;
   }
   return hipGetLastError();

@@ -267,3 +267,26 @@ def test_embed_lowrank_validation():
     assert bwd(g=g + 2) == 4 and bwd(nbytes=need - 1) == 9
     assert bwd(g=X0) == 5 and bwd(ws=tok) == 5
     assert bwd(N=0, dX=None) == 0
+
+
+def test_project_multi_validation():
+    L = sn.lib()
+    M = (ctypes.c_int64 * 3)(512, 256, 300)
+    need = L.sn_project_weights_multi_workspace_bytes(256, 8, 1, 3, M)
+    assert need >= L.sn_project_weights_workspace_bytes(256, 8, 1, 512)
+    assert L.sn_project_weights_multi_workspace_bytes(256, 8, 1, 17, M) == 0
+    W = (ctypes.c_void_p * 3)(FAKE + (1 << 24), FAKE + (2 << 24), FAKE + (3 << 24))
+    LD = (ctypes.c_int64 * 3)(512, 256, 300)
+    ws = FAKE + (8 << 24)
+
+    def call(count=3, Wp=W, Mp=M, LDp=LD, w=ws, nbytes=need):
+        return L.sn_project_weights_multi(FAKE, 256, 8, 1, count, Wp, Mp, LDp, w, nbytes, None)
+    assert call(count=17) == 2 and call(count=-1) == 2
+    assert call(Wp=None) == 1 and call(w=None) == 1
+    assert call(nbytes=need - 1) == 9 and call(w=ws + 64) == 4
+    bad_ld = (ctypes.c_int64 * 3)(512, 255, 300)
+    assert call(LDp=bad_ld) == 2
+    overlapping = (ctypes.c_void_p * 3)(FAKE + (1 << 24), FAKE + (1 << 24) + 1024, FAKE + (3 << 24))
+    assert call(Wp=overlapping) == 5
+    assert call(w=FAKE + (2 << 24)) == 5              # workspace overlaps W[1]
+    assert call(count=0) == 0

@@ -446,3 +446,36 @@ def test_deterministic_bitwise():
     x1 = host_bits(sn.sn_decompress(basis, Cin, tok=tok, E=E, P=P, seq_len=w["cfg"].seq))
     x2 = host_bits(sn.sn_decompress(basis, Cin, tok=tok, E=E, P=P, seq_len=w["cfg"].seq))
     assert np.array_equal(x1, x2)
+
+
+@pytest.mark.parametrize("dtype,d,k,widths,pad", [
+    ("bf16", 4096, 40, (4096, 14336), 0),      # config 2's Wo and W2 side by side
+    ("bf16", 512, 40, (256, 768, 512), 8),     # strided rows
+    ("bf16", 512, 40, (300, 512), 0),          # a width not a multiple of 256: one by one
+    ("bf16", 512, 100, (256, 512), 0),         # k > 64: one by one
+    ("f32", 256, 8, (256, 100), 0)])
+def test_project_weights_multi(dtype, d, k, widths, pad):
+    log(f"[project multi] {dtype} d={d} k={k} widths={widths} pad={pad}")
+    cfg = synth.Config("multi", dtype, d, k, 10, 1, 1, False, 0.0, 1.0)
+    b = synth.make_basis(0, cfg)
+    U = (oracle.decode_bf16(b["U"], np.float32) if dtype == "bf16" else b["U"]).astype(np.float64)
+    basis = sn.sn_basis_pack(dev(b["U"], dtype))
+    hosts, Ws = [], []
+    for i, m in enumerate(widths):
+        Wh = synth.make_weight(0, i, d, m, cfg)
+        hosts.append(Wh)
+        full = torch.zeros(d, m + pad, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32,
+                           device="cuda")
+        full[:, :m] = dev(Wh, dtype)
+        Ws.append(full[:, :m] if pad else full)
+    sn.sn_project_weights_multi(basis, Ws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(len(widths))
+    for i, (m, Wh) in enumerate(zip(widths, hosts)):
+        cols = np.unique(np.r_[0, m - 1, rng.integers(0, m, 40)])
+        Wf = (oracle.decode_bf16(Wh, np.float32) if dtype == "bf16" else Wh)[:, cols]
+        ref = oracle.round_to(oracle.project_weights(Wf.astype(np.float64), U), dtype)
+        got = host(Ws[i][:, torch.from_numpy(cols).cuda()])
+        assert_parity(got.T, ref.T, dtype, f"W[{i}] ({d}x{m}) sampled columns")
+        if pad:  # the padding columns are untouched
+            assert float(Ws[i].as_strided((d, pad), (m + pad, 1), m).abs().max()) == 0.0
