@@ -52,8 +52,11 @@ struct ProjPlan {
 
 // Pass 1 splits the rows of W into dsplit ranges when there are too few
 // column slabs to fill the chip; it picks the split that minimises
-// (rounds of workgroups) x (rows per workgroup) for `slots` resident
-// workgroups (slots <= 0: the largest split, for the workspace bound).
+// (rounds of workgroups) x (rows per workgroup + a fixed cost of 256 rows:
+// filling the load ring, the cross-wave reduction, the T writes) for `slots`
+// resident workgroups (slots <= 0: the largest split, for the workspace
+// bound).  Without the fixed cost, wide matrices were cut into many
+// workgroups of a few row steps each.
 ProjPlan proj_plan(int64_t k, int kt, int ks, int64_t m, int64_t d, int64_t slots) {
   ProjPlan P;
   P.m_pad = ceil_div(m, kPadCols) * kPadCols;
@@ -71,7 +74,7 @@ ProjPlan proj_plan(int64_t k, int kt, int ks, int64_t m, int64_t d, int64_t slot
   if (slots > 0) {
     for (int64_t ds = 1; ds <= max_ds; ++ds) {
       const int64_t rows = ceil_div(ceil_div(d, ds), 128) * 128;
-      const int64_t cost = ceil_div(slabs * ceil_div(d, rows), slots) * rows;
+      const int64_t cost = ceil_div(slabs * ceil_div(d, rows), slots) * (rows + 256);
       if (best_cost < 0 || cost < best_cost) {
         best = ds;
         best_cost = cost;
