@@ -48,13 +48,13 @@ CALIB_BYTES = 256 * 1024 * 1024   # plain copy used to scale the HBM counters
 
 # rocprofv3 kernel names of each op (substring match on the demangled name)
 OP_KERNELS = {
-    "compress": ["compress_kernel<3, true, true, true, 0>"],
+    "compress": ["compress_kernel<3, true, true, 8, 8, 0>"],
     "decompress": ["decompress_cb_kernel<2, true, true, 0>"],
-    "grad_compress": ["compress_kernel<3, false, false, false, 0>"],
+    "grad_compress": ["compress_kernel<3, false, false, 1, 8, 0>"],
     "grad_decompress": ["decompress_cb_kernel<2, false, false, 0>"],
-    "compress_projected": ["compress_kernel<3, false, false, false, 1>"],
+    "compress_projected": ["compress_kernel<3, false, false, 1, 8, 1>"],
     # subspace update: its compress pass and its contraction over tokens
-    "grassmann_compress": ["compress_kernel<3, false, false, false, 3>"],
+    "grassmann_compress": ["compress_kernel<3, false, false, 1, 8, 3>"],
     "grassmann_tokens": ["project_pass1_kernel<5, true, 8>"],
 }
 
@@ -66,7 +66,7 @@ GRASS_KERNELS = ["loss_kernel", "frag_kernel", "finish_kernel", "gram_partial_ke
                  "tiles_scan_kernel", "tile_write_kernel", "place_kernel",
                  "chunk_sum_kernel", "seg_sum_kernel",
                  "update_kernel", "chol_kernel", "tri_apply_kernel", "reset_kernel",
-                 "compress_kernel<3, false, false, false, 3>"]
+                 "compress_kernel<3, false, false, 1, 8, 3>"]
 
 
 def parse():
@@ -365,6 +365,20 @@ def _pair_times(sn, torch, basis, d, k, tok, E, P, seq, steps, R=2, grad=True):
         sn.sn_decompress(basis, Cs[j], out=Os[j])
 
     out = {"pair_ms": loop(fwd)}
+    # the pair's two kernels on their own: an event pair around each launch
+    mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))  # noqa: E731
+    evs = [(mk(), mk()) for _ in range(steps)]
+    for i, ((a, b), (c, e)) in enumerate(evs):
+        j = i % R
+        a.record(stream)
+        sn.sn_compress(basis, Xs[j], tok=tok, E=E, P=P, seq_len=seq, out=Cs[j])
+        b.record(stream)
+        c.record(stream)
+        sn.sn_decompress(basis, Cs[j], tok=tok, E=E, P=P, seq_len=seq, out=Os[j])
+        e.record(stream)
+    torch.cuda.synchronize()
+    out["compress_ms"] = float(np.mean([a.elapsed_time(b) for (a, b), _ in evs]))
+    out["decompress_ms"] = float(np.mean([c.elapsed_time(e) for _, (c, e) in evs]))
     if grad:
         out["grad_pair_ms"] = loop(bwd)
     del Xs, Cs, Os
@@ -406,6 +420,10 @@ def other_configs(sn, torch, steps: int) -> dict:
                 "pair_GBps": round(rate(pair_bytes, t["pair_ms"]), 1),
                 "pair_frac_hbm": round(rate(pair_bytes, t["pair_ms"]) / HBM_PEAK_GBS, 4),
                 "pair_tokens_per_s": round(N / (t["pair_ms"] * 1e-3), 1),
+                "compress_ms": round(t["compress_ms"], 5),
+                "decompress_ms": round(t["decompress_ms"], 5),
+                "decompress_frac_hbm": round(rate(pair_bytes / 2, t["decompress_ms"])
+                                             / HBM_PEAK_GBS, 4),
                 "grad_pair_ms": round(t["grad_pair_ms"], 5),
                 "grad_pair_GBps": round(rate(grad_bytes, t["grad_pair_ms"]), 1)}
         for i, (rows, cols) in enumerate(cfg.weights if cid == 4 else ()):
@@ -829,6 +847,23 @@ def main():
     pair_ms = pair_loop("compress")
     ppair_ms = pair_loop("compress_projected")
 
+    # Cold codec pair: before each iteration a 512 MB fill evicts the caches
+    # (the 256 MB Infinity Cache included), so compress finds none of X, E, P
+    # or U cached.  Median of the per-iteration times.
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cold = []
+    for i in range(max(5, K // 2)):
+        flush.fill_(i & 0xFF)
+        a, b = mk()
+        a.record(stream)
+        op("compress", i)
+        op("decompress", i)
+        b.record(stream)
+        cold.append((a, b))
+    torch.cuda.synchronize()
+    cold_ms = float(np.median([a.elapsed_time(b) for a, b in cold]))
+    del flush
+
     # the projected-table compress, back to back over the same buffer rotation
     # (the tables are rebuilt once, as after a subspace update)
     alt_samples = {"compress_projected": [], "embed_project": []}
@@ -891,7 +926,9 @@ def main():
                        "GBps": round(rate(pair_bytes, pair_ms), 1),
                        "frac_hbm": round(rate(pair_bytes, pair_ms) / HBM_PEAK_GBS, 4),
                        "tokens_per_s": round(N / (pair_ms * 1e-3), 1),
-                       "x_c_only_GBps": round(rate(2 * (xb + cb), pair_ms), 1)},
+                       "x_c_only_GBps": round(rate(2 * (xb + cb), pair_ms), 1),
+                       "cold_ms_median": round(cold_ms, 5),
+                       "cold_GBps": round(rate(pair_bytes, cold_ms), 1)},
         "codec_pair_projected": {
             "ops": "compress_projected+decompress, back to back (tables built once per basis)",
             "ms": round(ppair_ms, 5), "GBps": round(rate(ppair_bytes, ppair_ms), 1),

@@ -8,11 +8,12 @@
 //            is exact and every sum is fp32.
 // Without tables this is the gradient compress of Sec. 4.4.
 //
-// compress_kernel (one workgroup = 4 compute waves + 3 producer waves, 64 tokens):
+// compress_kernel (one workgroup = NW compute waves + 3 producer waves, 16 NW
+// tokens; NW = 8 where four stage buffers still fit in LDS, else 4):
 //
 // * Three producer waves copy, for each stage of 64 columns of d, everything
 //   the compute waves need into one of NB LDS buffers with direct-to-LDS
-//   loads: wave A the 64 tokens' X rows, wave B their T_fixed and P rows,
+//   loads: wave A the tokens' X rows, wave B their T_fixed and P rows,
 //   wave C the U fragments of the stage.  Each copy instruction reads 8 rows
 //   x 128 contiguous bytes (contiguous row pieces are much cheaper for the
 //   memory pipeline than the 16-rows-x-64-bytes pattern of an MFMA operand),
@@ -22,15 +23,17 @@
 // * Compute wave w owns 16 tokens and the whole of d; it reads operands only
 //   from LDS (no global loads in its main loop), so nothing stalls it but the
 //   hand-over barrier.
-// * NB-deep buffering (NB = 6 at k <= 48): the copies keep NB - 1 stages in
-//   flight, which is what sets the kernel's speed (one workgroup per CU);
-//   three producers keep each wave's outstanding copies within the 6-bit
-//   vmcnt range.  One barrier per stage hands a buffer over.  Workgroups
-//   start at different stages (rotation) so the rows in flight across the
-//   chip are not read at the same column offsets.
+// * NB-deep buffering (as many stage buffers as LDS holds, at most 6): the
+//   copies keep NB - 1 stages in flight, which is what sets the kernel's
+//   speed (one workgroup per CU); three producers keep each wave's
+//   outstanding copies within the 6-bit vmcnt range.  One barrier per stage
+//   hands a buffer over.  Workgroups start at different stages (rotation) so
+//   the rows in flight across the chip are not read at the same column
+//   offsets.  The U fragments of a stage are copied once per workgroup, so
+//   eight compute waves (128 tokens) halve their share of the copies.
 // * Position-major tiles (positions i mod seq_len, batch a multiple of 4): a
-//   16-token tile holds 16/B consecutive positions of B batches, so the tile
-//   needs only 16/B positional rows.
+//   16-token tile holds 16/BP consecutive positions of BP batches, so the
+//   tile needs only 16/BP positional rows.
 //
 // stream_compress_kernel (X U with no gathered rows) is described at its
 // definition.
@@ -40,15 +43,17 @@ namespace sn {
 
 namespace {
 
-constexpr int kW = 4;                  // compute waves per workgroup
+constexpr int kW = 4;                  // compute waves per workgroup (streaming kernel)
 constexpr int kThreads = 64 * (kW + 1);
-constexpr int kTokens = 16 * kW;       // tokens per workgroup
 constexpr int kStageCols = 64;         // d-elements per stage
 constexpr int kPieces = 8;             // 16-byte pieces per row per stage
 constexpr int kRowsPerCopy = 64 / kPieces;  // rows per direct-to-LDS copy instruction
 constexpr int kProd = 3;               // producer waves of compress_kernel
-constexpr int kThreadsC = 64 * (kW + kProd);
 constexpr int kMaxStages = 6;
+
+// threads of a compress_kernel workgroup with NW compute waves
+template <int NW>
+constexpr int threads_c() { return 64 * (NW + kProd); }
 constexpr int kLdsBytes = 160 * 1024;
 
 // 16-byte LDS slot of piece p of row r in a row tile.
@@ -81,27 +86,30 @@ __device__ __forceinline__ int64_t tile_pos0(const Tiling &tm, int64_t T) {
   return (T % tpb) * pg;
 }
 
-template <bool PM>
-constexpr int p_rows() { return PM ? 16 : kTokens; }  // positional rows staged per workgroup
+// positional rows staged per workgroup: 16/BP per tile in position-major
+// order (BP batches per tile), one per token in token-major order (BP = 1)
+template <int NW, int BP>
+constexpr int p_rows() { return BP > 1 ? NW * (16 / BP) : 16 * NW; }
 
 // ---------------------------------------------------------------------------
 // Stage buffer geometry (in 16-byte units) of compress_kernel.
 // ---------------------------------------------------------------------------
-template <int KT, bool HE, bool HP, bool PM>
+template <int KT, bool HE, bool HP, int BP, int NW>
 struct CGeo {
+  static constexpr int tokens = 16 * NW;
   static constexpr int x_off = 0;
-  static constexpr int e_off = x_off + kTokens * kPieces;
-  static constexpr int p_off = e_off + (HE ? kTokens * kPieces : 0);
-  static constexpr int u_off = p_off + (HP ? p_rows<PM>() * kPieces : 0);
+  static constexpr int e_off = x_off + tokens * kPieces;
+  static constexpr int p_off = e_off + (HE ? tokens * kPieces : 0);
+  static constexpr int u_off = p_off + (HP ? p_rows<NW, BP>() * kPieces : 0);
   static constexpr int u_frags = (kStageCols / 32) * KT;
   static constexpr int buf_units = u_off + u_frags * 64;
   // with both tables, the positional rows go with the U fragments so the
   // three producers issue about as many copies each
   static constexpr bool p_with_u = HE && HP;
   // copy instructions per stage of each producer: X; gathered rows; U
-  static constexpr int dma_a = kTokens / kRowsPerCopy;
-  static constexpr int dma_p = HP ? p_rows<PM>() / kRowsPerCopy : 0;
-  static constexpr int dma_b = (HE ? kTokens / kRowsPerCopy : 0) + (p_with_u ? 0 : dma_p);
+  static constexpr int dma_a = tokens / kRowsPerCopy;
+  static constexpr int dma_p = HP ? (p_rows<NW, BP>() + kRowsPerCopy - 1) / kRowsPerCopy : 0;
+  static constexpr int dma_b = (HE ? tokens / kRowsPerCopy : 0) + (p_with_u ? 0 : dma_p);
   static constexpr int dma_c = u_frags + (p_with_u ? dma_p : 0);
   static constexpr int dmax = dma_a > dma_b ? (dma_a > dma_c ? dma_a : dma_c)
                                             : (dma_b > dma_c ? dma_b : dma_c);
@@ -112,6 +120,15 @@ struct CGeo {
   static constexpr int nb = nb_cap - 2 > 63 / dmax ? 2 + 63 / dmax : nb_cap;
   static_assert(nb >= 3, "at least two stages in flight");
 };
+
+// Compute waves per workgroup: 8 while four stage buffers of that width fit
+// in LDS, else 4.
+template <int KT, bool HE, bool HP, int BP>
+constexpr int nw_of() {
+  constexpr int rows = 128 * (HE ? 2 : 1) + (HP ? p_rows<8, BP>() : 0);  // X, T_fixed, P rows
+  constexpr int units = rows * kPieces + (kStageCols / 32) * KT * 64;
+  return kLdsBytes / (units * 16) >= 4 ? 8 : 4;
+}
 
 // ---------------------------------------------------------------------------
 // Producer waves
@@ -173,15 +190,17 @@ __device__ __forceinline__ void wait_stages(int later) {
 // off-subspace loss, plus the bf16 coefficients when an output is given.
 enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2, kEpiGrass = 3 };
 
-template <int KT, bool HE, bool HP, bool PM, int EPI>
-__global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__restrict__ kfrag,
+template <int KT, bool HE, bool HP, int BP, int NW, int EPI>
+__global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t *__restrict__ kfrag,
                                                              int64_t d, int64_t k,
                                                              const bf16_t *__restrict__ X,
                                                              int64_t ldx, Tiling tm, IdArgs ids,
                                                              ProjArgs pa, void *__restrict__ Cout,
                                                              int64_t ldc, int cvec, GrassOut go) {
-  static_assert(EPI == kEpiBf16 || (!HE && !HP && !PM), "projected epilogues have no tables");
-  using G = CGeo<KT, HE, HP, PM>;
+  static_assert(EPI == kEpiBf16 || (!HE && !HP && BP == 1), "projected epilogues have no tables");
+  constexpr bool PM = BP > 1;
+  constexpr int kTokens = 16 * NW;
+  using G = CGeo<KT, HE, HP, BP, NW>;
   constexpr int NB = G::nb;
   __shared__ u32x4 lds[NB * G::buf_units];
 
@@ -191,16 +210,16 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
   const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nst));
   auto phys = [&](int si) { const int v = si + rot; return v >= nst ? v - nst : v; };
   const int64_t ntiles = (tm.N + 15) / 16;
-  const int64_t T0 = static_cast<int64_t>(blockIdx.x) * kW;
+  const int64_t T0 = static_cast<int64_t>(blockIdx.x) * NW;
 
-  if (wave >= kW) {  // ------------------------------------------------ producers
+  if (wave >= NW) {  // ------------------------------------------------ producers
     // 0: X rows; 1: T_fixed rows (and P rows with no T_fixed); 2: U fragments
     // (and P rows with both tables)
-    const int role = wave - kW;
+    const int role = wave - NW;
     const int prole = G::p_with_u ? 2 : 1;  // the producer that copies P rows
     const int q = lane / kPieces, m = lane % kPieces;
     RowSet<kTokens> rx, re;
-    RowSet<p_rows<PM>()> rp;
+    RowSet<G::dma_p * kRowsPerCopy> rp;
     // token row r = 16 w + n of the workgroup (tiles past the end repeat the last)
     auto token_of = [&](int r) {
       int64_t T = T0 + r / 16;
@@ -229,13 +248,13 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
           rp.ptr[i] = row_ptr(ids.P, ids.ldp, ps);
         }
       } else {
-        // positional row r = w * pg + rho of the workgroup (rows past 4 pg
+        // positional row r = w * pg + rho of the workgroup (rows past NW pg
         // repeat the last one so the copy count stays fixed)
-        const int pg = 16 / tm.bp;
+        constexpr int pg = 16 / BP;
 #pragma unroll
-        for (int i = 0; i < p_rows<PM>() / kRowsPerCopy; ++i) {
+        for (int i = 0; i < G::dma_p; ++i) {
           int r = kRowsPerCopy * i + q;
-          r = r < kW * pg ? r : kW * pg - 1;
+          r = r < NW * pg ? r : NW * pg - 1;
           int64_t T = T0 + r / pg;
           T = T < ntiles ? T : ntiles - 1;
           rp.ptr[i] = row_ptr(ids.P, ids.ldp, tile_pos0(tm, T) + r % pg);
@@ -280,7 +299,7 @@ __global__ __launch_bounds__(kThreadsC) void compress_kernel(const bf16_t *__res
   // ------------------------------------------------------------ compute waves
   const int g = lane >> 4, n = lane & 15;
   const int xrow = 16 * wave + n;
-  const int prow = PM ? wave * (16 / tm.bp) + n / tm.bp : xrow;
+  const int prow = PM ? wave * (16 / BP) + n / BP : xrow;
 
   f32x4 acc[KT];
 #pragma unroll
@@ -536,15 +555,16 @@ bool tables_ok(const IdArgs &ids) {
 }
 
 // Position-major tiling when the positions are the default i mod seq_len of a
-// row-major [batch, seq_len] batch with batch a multiple of 4 (8 preferred).
-Tiling pick_tiling(int64_t N, const IdArgs &ids) {
+// row-major [batch, seq_len] batch with batch a multiple of 4 (8 preferred)
+// and whole workgroups of nw tiles.
+Tiling pick_tiling(int64_t N, const IdArgs &ids, int nw) {
   Tiling tm{N, 1, 1};
   if (!ids.P || ids.pos || ids.seq_len <= 0 || N % ids.seq_len != 0) return tm;
   const int64_t batch = N / ids.seq_len;
   for (int bp : {8, 4}) {
     const int pg = 16 / bp;
-    // every workgroup holds 4 full tiles: N / 16 must be a multiple of 4
-    if (batch % bp == 0 && ids.seq_len % pg == 0 && (N / 16) % kW == 0) {
+    // every workgroup holds nw full tiles: N / 16 must be a multiple of nw
+    if (batch % bp == 0 && ids.seq_len % pg == 0 && N % 16 == 0 && (N / 16) % nw == 0) {
       tm.seq = ids.seq_len;
       tm.bp = bp;
       return tm;
@@ -553,13 +573,14 @@ Tiling pick_tiling(int64_t N, const IdArgs &ids) {
   return tm;
 }
 
-template <int KT, bool HE, bool HP, bool PM, int EPI = kEpiBf16>
+template <int KT, bool HE, bool HP, int BP, int EPI = kEpiBf16>
 void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx, const Tiling &tm,
               const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s,
               const ProjArgs &pa = ProjArgs{}, const GrassOut &go = GrassOut{}) {
+  constexpr int NW = nw_of<KT, HE, HP, BP>();
   const int64_t ntiles = (tm.N + 15) / 16;
-  dim3 grid(static_cast<unsigned>(ceil_div(ntiles, kW)));
-  compress_kernel<KT, HE, HP, PM, EPI><<<grid, kThreadsC, 0, s>>>(
+  dim3 grid(static_cast<unsigned>(ceil_div(ntiles, NW)));
+  compress_kernel<KT, HE, HP, BP, NW, EPI><<<grid, threads_c<NW>(), 0, s>>>(
       kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec, go);
 }
 
@@ -573,14 +594,14 @@ hipError_t launch_plain_kt(const PackLayout &L, const void *packed, const void *
   const Tiling tm{N, 1, 1};
   const IdArgs none{};
   switch (L.kt) {
-    case 1: launch_c<1, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 2: launch_c<2, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 3: launch_c<3, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 4: launch_c<4, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 5: launch_c<5, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 6: launch_c<6, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 7: launch_c<7, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
-    case 8: launch_c<8, false, false, false, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 1: launch_c<1, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 2: launch_c<2, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 3: launch_c<3, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 4: launch_c<4, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 5: launch_c<5, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 6: launch_c<6, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 7: launch_c<7, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
+    case 8: launch_c<8, false, false, 1, EPI>(kf, L, X, ldx, tm, none, C, ldc, cvec, s, pa); break;
     default: return hipErrorNotSupported;
   }
   return hipGetLastError();
@@ -599,19 +620,29 @@ template <int KT>
 void launch_c_kt(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx,
                  const Tiling &tm, const IdArgs &ids, void *C, int64_t ldc, int cvec,
                  hipStream_t s) {
-  const bool he = ids.E != nullptr, hp = ids.P != nullptr, pm = tm.bp != 1;
-  if (he && hp && pm)
-    launch_c<KT, true, true, true>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
-  else if (he && hp)
-    launch_c<KT, true, true, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
-  else if (he)
-    launch_c<KT, true, false, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
-  else if (hp && pm)
-    launch_c<KT, false, true, true>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
-  else if (hp)
-    launch_c<KT, false, true, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
-  else
-    launch_c<KT, false, false, false>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  const bool he = ids.E != nullptr, hp = ids.P != nullptr;
+  if (he && hp) {
+    // position-major tiles when whole workgroups of tiles allow them
+    const Tiling tm8 = pick_tiling(tm.N, ids, nw_of<KT, true, true, 8>());
+    const Tiling tm4 = pick_tiling(tm.N, ids, nw_of<KT, true, true, 4>());
+    if (tm8.bp == 8)
+      launch_c<KT, true, true, 8>(kf, L, X, ldx, tm8, ids, C, ldc, cvec, s);
+    else if (tm4.bp == 4)
+      launch_c<KT, true, true, 4>(kf, L, X, ldx, tm4, ids, C, ldc, cvec, s);
+    else
+      launch_c<KT, true, true, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  } else if (he) {
+    launch_c<KT, true, false, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  } else {
+    const Tiling tm8 = pick_tiling(tm.N, ids, nw_of<KT, false, true, 8>());
+    const Tiling tm4 = pick_tiling(tm.N, ids, nw_of<KT, false, true, 4>());
+    if (tm8.bp == 8)
+      launch_c<KT, false, true, 8>(kf, L, X, ldx, tm8, ids, C, ldc, cvec, s);
+    else if (tm4.bp == 4)
+      launch_c<KT, false, true, 4>(kf, L, X, ldx, tm4, ids, C, ldc, cvec, s);
+    else
+      launch_c<KT, false, true, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+  }
 }
 
 }  // namespace
@@ -628,7 +659,7 @@ hipError_t launch_compress_mfma(const PackLayout &L, const void *packed, const v
       reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_kfrag);
   const int cvec = ((reinterpret_cast<uintptr_t>(C) & 7) == 0) && (ldc % 4 == 0);
   if (!ids.E && !ids.P) return launch_plain<kEpiBf16>(L, packed, X, N, ldx, ProjArgs{}, C, ldc, s);
-  const Tiling tm = pick_tiling(N, ids);
+  const Tiling tm{N, 1, 1};  // token-major; the table dispatch picks position-major tiles
   switch (L.kt) {
     case 1: launch_c_kt<1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
     case 2: launch_c_kt<2>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s); break;
@@ -670,14 +701,14 @@ hipError_t launch_grass_compress_mfma(const PackLayout &L, const void *packed, c
   const IdArgs none{};
   const ProjArgs pa{};
   switch (L.kt) {
-    case 1: launch_c<1, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 2: launch_c<2, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 3: launch_c<3, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 4: launch_c<4, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 5: launch_c<5, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 6: launch_c<6, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 7: launch_c<7, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
-    case 8: launch_c<8, false, false, false, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 1: launch_c<1, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 2: launch_c<2, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 3: launch_c<3, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 4: launch_c<4, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 5: launch_c<5, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 6: launch_c<6, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 7: launch_c<7, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
+    case 8: launch_c<8, false, false, 1, kEpiGrass>(kf, L, G, ldg, tm, none, Cwire, ldc, cvec, s, pa, go); break;
     default: return hipErrorNotSupported;
   }
   return hipGetLastError();
