@@ -20,6 +20,10 @@
 //   and the 16-byte pieces of row r are stored in the order p ^ (r & 7) so
 //   that the compute waves' operand reads (16 rows, same piece) spread over
 //   the banks.
+// * T_fixed rows are copied once per distinct id of the workgroup's tokens
+//   (Zipf-distributed ids repeat: about 80 distinct ids per 128 tokens at
+//   vocab 32000); the T_fixed producer finds the distinct ids at the start
+//   and hands each compute lane the slot of its token's row.
 // * Compute wave w owns 16 tokens and the whole of d; it reads operands only
 //   from LDS (no global loads in its main loop), so nothing stalls it but the
 //   hand-over barrier.
@@ -154,6 +158,21 @@ __device__ __forceinline__ void dma_rows(const RowSet<R> &rs, int64_t col, u32x4
   }
 }
 
+// The first n (wave-uniform) copies of dma_rows.
+template <int R>
+__device__ __forceinline__ void dma_rows_n(const RowSet<R> &rs, int n, int64_t col, u32x4 *dst,
+                                           int q, int m) {
+#pragma unroll
+  for (int i = 0; i < R / kRowsPerCopy; ++i) {
+    if (i < n) {
+      const int r = kRowsPerCopy * i + q;
+      __builtin_amdgcn_global_load_lds(
+          static_cast<const void *>(rs.ptr[i] + col + 8 * (m ^ (r & 7))),
+          (__attribute__((address_space(3))) void *)(dst + i * 64), 16, 0, 0);
+    }
+  }
+}
+
 __device__ __forceinline__ void dma_frags(const bf16_t *src, int frags, u32x4 *dst, int lane) {
   for (int f = 0; f < frags; ++f) lds_dma_16(src + f * 512 + lane * 8, dst + f * 64);
 }
@@ -173,6 +192,20 @@ __device__ __forceinline__ void wait_stages(int later) {
       return;
     }
     wait_stages<PER, L - 1>(later);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+// Wait until at most v (wave-uniform, 0 <= v <= V) copies are outstanding.
+template <int V>
+__device__ __forceinline__ void wait_vm_upto(int v) {
+  if constexpr (V > 0) {
+    if (v >= V) {
+      wait_vmcnt<V>();
+      return;
+    }
+    wait_vm_upto<V - 1>(v);
   } else {
     wait_vmcnt<0>();
   }
@@ -231,11 +264,61 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
       for (int i = 0; i < kTokens / kRowsPerCopy; ++i)
         rx.ptr[i] = X + token_of(kRowsPerCopy * i + q) * ldx;
     }
+    // T_fixed copies per stage: one per 8 distinct ids
+    int ce = G::dma_b;
     if (role == 1 && HE) {
+      static_assert(kTokens == 128 || kTokens == 64, "one or two tokens per lane");
+      constexpr int TPL = kTokens / 64;  // tokens per lane
+      // scratch in the last stage buffer, which no copy touches before the
+      // first stage hand-over: ids, slot of each first occurrence, distinct
+      // ids in slot order, and each token's slot (read by the compute waves)
+      int *scr = reinterpret_cast<int *>(lds + (NB - 1) * G::buf_units + G::e_off);
+      int *sid = scr, *sfirst = scr + kTokens, *surow = scr + 2 * kTokens;
+      int *smap = scr + 3 * kTokens;
+      int id[TPL], f[TPL];
+#pragma unroll
+      for (int h = 0; h < TPL; ++h) {
+        const int64_t t = token_of(lane + 64 * h);
+        id[h] = static_cast<int>(clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1));
+        sid[lane + 64 * h] = id[h];
+        f[h] = lane + 64 * h;
+      }
+      // first occurrence of each token's id (same wave: the writes above are
+      // visible to these reads)
+      for (int j = 0; j < kTokens; j += 4) {
+        const int4 v = *reinterpret_cast<const int4 *>(sid + j);
+#pragma unroll
+        for (int h = 0; h < TPL; ++h) {
+          // scanning upwards, the first match is the smallest index
+          if (v.w == id[h] && j + 3 < f[h]) f[h] = j + 3;
+          if (v.z == id[h] && j + 2 < f[h]) f[h] = j + 2;
+          if (v.y == id[h] && j + 1 < f[h]) f[h] = j + 1;
+          if (v.x == id[h] && j < f[h]) f[h] = j;
+        }
+      }
+      // slots in token order of the first occurrences
+      const uint64_t below = (1ull << lane) - 1ull;
+      int u = 0;
+#pragma unroll
+      for (int h = 0; h < TPL; ++h) {
+        const bool first = f[h] == lane + 64 * h;
+        const uint64_t mk = __ballot(first);
+        const int sl = u + __popcll(mk & below);
+        if (first) {
+          sfirst[lane + 64 * h] = sl;
+          surow[sl] = id[h];
+        }
+        u += __popcll(mk);
+      }
+#pragma unroll
+      for (int h = 0; h < TPL; ++h) smap[lane + 64 * h] = sfirst[f[h]];
+      u = __builtin_amdgcn_readfirstlane(u);
+      ce = (u + kRowsPerCopy - 1) / kRowsPerCopy;
 #pragma unroll
       for (int i = 0; i < kTokens / kRowsPerCopy; ++i) {
-        const int64_t t = token_of(kRowsPerCopy * i + q);
-        re.ptr[i] = row_ptr(ids.E, ids.lde, clamp_id(ids.tok[t], ids.vocab, ids.err_flag, 1));
+        int r = kRowsPerCopy * i + q;
+        r = r < u ? r : u - 1;  // lanes of a part-filled last copy repeat the last row
+        re.ptr[i] = row_ptr(ids.E, ids.lde, surow[r]);
       }
     }
     if (role == prole && HP) {
@@ -270,7 +353,7 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
         // second pass reads G in reverse order, from the Infinity Cache)
         dma_rows<kTokens, EPI != kEpiGrass>(rx, col, b + G::x_off, q, m);
       } else if (role == 1) {
-        if (HE) dma_rows(re, col, b + G::e_off, q, m);
+        if (HE) dma_rows_n(re, ce, col, b + G::e_off, q, m);
         if (HP && !G::p_with_u) dma_rows(rp, col, b + G::p_off, q, m);
       } else {
         dma_frags(kfrag + static_cast<int64_t>(st) * G::u_frags * 512, G::u_frags, b + G::u_off,
@@ -280,12 +363,15 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
     };
     for (int s = 0; s < NB - 1; ++s)
       if (s < nst) issue(s);
+    if (HE) lds_barrier();  // the token slots are in LDS
     for (int s = 0; s < nst; ++s) {
       // stage s has landed once at most the later stages in flight are pending
       int later = nst - 1 - s;
       later = later < NB - 2 ? later : NB - 2;
       if (role == 0)
         wait_stages<G::dma_a, NB - 2>(later);
+      else if (role == 1 && HE)
+        wait_vm_upto<G::dma_b * (NB - 2)>(later * ce);
       else if (role == 1)
         wait_stages<G::dma_b, NB - 2>(later);
       else
@@ -300,6 +386,11 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
   const int g = lane >> 4, n = lane & 15;
   const int xrow = 16 * wave + n;
   const int prow = PM ? wave * (16 / BP) + n / BP : xrow;
+  int erow = xrow;  // slot of the token's T_fixed row
+  if constexpr (HE) {
+    lds_barrier();
+    erow = reinterpret_cast<const int *>(lds + (NB - 1) * G::buf_units + G::e_off)[3 * kTokens + xrow];
+  }
 
   f32x4 acc[KT];
 #pragma unroll
@@ -326,7 +417,7 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
         sq += static_cast<double>(s8);
       }
       u32x4 be, bpv;
-      if (HE) be = neg8(b[G::e_off + slot(xrow, pc)]);
+      if (HE) be = neg8(b[G::e_off + slot(erow, pc)]);
       if (HP) bpv = neg8(b[G::p_off + slot(prow, pc)]);
 #pragma unroll
       for (int t = 0; t < KT; ++t) {
