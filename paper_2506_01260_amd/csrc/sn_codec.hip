@@ -9,7 +9,8 @@
 // Without tables this is the gradient compress of Sec. 4.4.
 //
 // compress_kernel (one workgroup = NW compute waves + 3 producer waves, 16 NW
-// tokens; NW = 8 where four stage buffers still fit in LDS, else 4):
+// tokens; NW = 8 where four stage buffers still fit in LDS and the launch
+// has a workgroup for every CU, else 4):
 //
 // * Three producer waves copy, for each stage of 64 columns of d, everything
 //   the compute waves need into one of NB LDS buffers with direct-to-LDS
@@ -648,31 +649,56 @@ bool tables_ok(const IdArgs &ids) {
 // Position-major tiling when the positions are the default i mod seq_len of a
 // row-major [batch, seq_len] batch with batch a multiple of 4 (8 preferred)
 // and whole workgroups of nw tiles.
-Tiling pick_tiling(int64_t N, const IdArgs &ids, int nw) {
-  Tiling tm{N, 1, 1};
-  if (!ids.P || ids.pos || ids.seq_len <= 0 || N % ids.seq_len != 0) return tm;
+bool pm_tiling_ok(int64_t N, const IdArgs &ids, int bp, int nw) {
+  if (!ids.P || ids.pos || ids.seq_len <= 0 || N % ids.seq_len != 0 || N % 16 != 0) return false;
   const int64_t batch = N / ids.seq_len;
-  for (int bp : {8, 4}) {
-    const int pg = 16 / bp;
-    // every workgroup holds nw full tiles: N / 16 must be a multiple of nw
-    if (batch % bp == 0 && ids.seq_len % pg == 0 && N % 16 == 0 && (N / 16) % nw == 0) {
-      tm.seq = ids.seq_len;
-      tm.bp = bp;
-      return tm;
-    }
+  // every workgroup holds nw full tiles: N / 16 must be a multiple of nw
+  return batch % bp == 0 && ids.seq_len % (16 / bp) == 0 && (N / 16) % nw == 0;
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int c = 0;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c <= 0)
+      c = 256;
+    cached[dev] = c;
   }
-  return tm;
+  return cached[dev];
+}
+
+// Compute waves of a launch over N tokens: 8 where the stage buffers allow
+// it and the launch still has a workgroup for every CU, else 4 (a launch of
+// fewer, wider workgroups would leave CUs idle).
+template <int KT, bool HE, bool HP, int BP>
+int pick_nw(int64_t N) {
+  if constexpr (nw_of<KT, HE, HP, BP>() != 8) {
+    return 4;
+  } else {
+    return ceil_div(ceil_div(N, 16), 8) >= device_cus() ? 8 : 4;
+  }
 }
 
 template <int KT, bool HE, bool HP, int BP, int EPI = kEpiBf16>
 void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx, const Tiling &tm,
               const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s,
               const ProjArgs &pa = ProjArgs{}, const GrassOut &go = GrassOut{}) {
-  constexpr int NW = nw_of<KT, HE, HP, BP>();
   const int64_t ntiles = (tm.N + 15) / 16;
-  dim3 grid(static_cast<unsigned>(ceil_div(ntiles, NW)));
-  compress_kernel<KT, HE, HP, BP, NW, EPI><<<grid, threads_c<NW>(), 0, s>>>(
-      kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec, go);
+  if constexpr (nw_of<KT, HE, HP, BP>() == 8) {
+    if (pick_nw<KT, HE, HP, BP>(tm.N) == 8) {
+      compress_kernel<KT, HE, HP, BP, 8, EPI>
+          <<<dim3(static_cast<unsigned>(ceil_div(ntiles, 8))), threads_c<8>(), 0, s>>>(
+              kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec, go);
+      return;
+    }
+  }
+  compress_kernel<KT, HE, HP, BP, 4, EPI>
+      <<<dim3(static_cast<unsigned>(ceil_div(ntiles, 4))), threads_c<4>(), 0, s>>>(
+          kf, L.d, L.k, static_cast<const bf16_t *>(X), ldx, tm, ids, pa, C, ldc, cvec, go);
 }
 
 // X U with no gathered rows, on the staged kernel (d a multiple of kStageCols)
@@ -712,24 +738,23 @@ void launch_c_kt(const bf16_t *kf, const PackLayout &L, const void *X, int64_t l
                  const Tiling &tm, const IdArgs &ids, void *C, int64_t ldc, int cvec,
                  hipStream_t s) {
   const bool he = ids.E != nullptr, hp = ids.P != nullptr;
+  const int64_t N = tm.N;
+  // position-major tiles (8 batches per tile, else 4) when whole workgroups
+  // of tiles allow them
+  const Tiling tm8{N, ids.seq_len, 8}, tm4{N, ids.seq_len, 4};
   if (he && hp) {
-    // position-major tiles when whole workgroups of tiles allow them
-    const Tiling tm8 = pick_tiling(tm.N, ids, nw_of<KT, true, true, 8>());
-    const Tiling tm4 = pick_tiling(tm.N, ids, nw_of<KT, true, true, 4>());
-    if (tm8.bp == 8)
+    if (pm_tiling_ok(N, ids, 8, pick_nw<KT, true, true, 8>(N)))
       launch_c<KT, true, true, 8>(kf, L, X, ldx, tm8, ids, C, ldc, cvec, s);
-    else if (tm4.bp == 4)
+    else if (pm_tiling_ok(N, ids, 4, pick_nw<KT, true, true, 4>(N)))
       launch_c<KT, true, true, 4>(kf, L, X, ldx, tm4, ids, C, ldc, cvec, s);
     else
       launch_c<KT, true, true, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
   } else if (he) {
     launch_c<KT, true, false, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
   } else {
-    const Tiling tm8 = pick_tiling(tm.N, ids, nw_of<KT, false, true, 8>());
-    const Tiling tm4 = pick_tiling(tm.N, ids, nw_of<KT, false, true, 4>());
-    if (tm8.bp == 8)
+    if (pm_tiling_ok(N, ids, 8, pick_nw<KT, false, true, 8>(N)))
       launch_c<KT, false, true, 8>(kf, L, X, ldx, tm8, ids, C, ldc, cvec, s);
-    else if (tm4.bp == 4)
+    else if (pm_tiling_ok(N, ids, 4, pick_nw<KT, false, true, 4>(N)))
       launch_c<KT, false, true, 4>(kf, L, X, ldx, tm4, ids, C, ldc, cvec, s);
     else
       launch_c<KT, false, true, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);

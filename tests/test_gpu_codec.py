@@ -372,6 +372,35 @@ def test_out_of_range_ids_are_clamped_and_flagged(dtype):
                                             dtype), dtype, "decompress with clamped ids")
 
 
+@pytest.mark.parametrize("pattern", ["one id", "all distinct", "two ids", "zipf"])
+@pytest.mark.parametrize("n,seq", [(512, 64), (500, 50), (1024, 32)])
+def test_compress_token_id_patterns(pattern, n, seq):
+    """The compress copies each distinct T_fixed row of a workgroup once and
+    maps every token to its row: ids that all repeat, never repeat, alternate,
+    or follow Zipf, in position-major (n = batch x seq, batch 8 or 32) and
+    token-major (500 tokens) order."""
+    d, k, vocab = 512, 40, 700
+    log(f"[id patterns] {pattern} n={n} seq={seq}")
+    rng = np.random.default_rng(n + len(pattern))
+    U, _ = np.linalg.qr(rng.standard_normal((d, k)))
+    E = rng.standard_normal((vocab, d)) * 0.05
+    P = rng.standard_normal((seq, d)) * 0.05
+    tok = {"one id": np.full(n, 17),
+           "all distinct": rng.permutation(vocab)[:n] if n <= vocab else np.arange(n) % vocab,
+           "two ids": np.where(np.arange(n) % 2 == 0, 3, vocab - 1),
+           "zipf": np.minimum(rng.zipf(1.1, n), vocab) - 1}[pattern].astype(np.int32)
+    pos = (np.arange(n) % seq).astype(np.int32)
+    X = E[tok] + P[pos] + rng.standard_normal((n, d)) * 0.05
+    st = {nm: synth.store(a, "bf16") for nm, a in dict(U=U, E=E, P=P, X=X).items()}
+    f64 = {nm: oracle.decode_bf16(a) for nm, a in st.items()}
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    C = sn.sn_compress(basis, dev(st["X"], "bf16"), tok=ids(tok), E=dev(st["E"], "bf16"),
+                       P=dev(st["P"], "bf16"), seq_len=seq)
+    ref = oracle.round_to(oracle.compress(f64["X"], f64["U"], tok, f64["E"], f64["P"],
+                                          seq_len=seq), "bf16")
+    assert_parity(host(C), ref, "bf16", f"compress, {pattern}")
+
+
 def test_bit_exact_gather_and_subtract():
     """C = 0 decompresses to exactly E[tok] + P[pos]; X = E[tok] + P[pos]
     compresses to exactly 0 (values on a grid where every sum is exact)."""
