@@ -591,7 +591,7 @@ def adamw_times(sn, torch, weights, steps: int) -> dict:
             b.record(stream)
             torch.cuda.synchronize()
             ms = a.elapsed_time(b) / steps
-            # read G, M, V, W and write M, V, W once each (the subspace form reads M twice)
+            # read G, M, V, W and write M, V, W once each (the subspace form reads G twice)
             nbytes = rows * cols * (2 + 4 + 4 + 2 + 4 + 4 + 2)
             res[name] = {"ms": round(ms, 5), "bytes": nbytes,
                          "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),

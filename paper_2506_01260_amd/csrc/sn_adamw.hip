@@ -13,10 +13,11 @@
 // App. A): no projection is needed for W_p2.
 //
 // Memory-bound.  A thread owns 8 consecutive columns (16-byte loads of bf16
-// G / W, 32-byte loads of M and V) over kRows rows.  Standard: one pass.
-// Subspace: pass 1 updates M and V and writes per-block column sums of V;
-// pass 2 adds the blocks in a fixed order and forms alpha; pass 3 reads M
-// again and updates W.
+// G / W, 32-byte loads of M and V) over kRows rows.  Standard: one pass
+// (22 bytes per bf16 element).  Subspace: pass 1 updates V and writes
+// per-block column sums of it; pass 2 adds the blocks in a fixed order and
+// forms alpha; pass 3 reads G again, updates M and W (24 bytes per element:
+// G is read twice, M once).
 #include "sn_device.h"
 #include "sn_internal.h"
 
@@ -86,8 +87,9 @@ __device__ __forceinline__ void store8(T *row, int64_t c0, int64_t cols, const f
   }
 }
 
-// Pass 1 (and the whole standard step when !SUB): moments, then either the
-// column sums of the new V (SUB) or the W update with the entrywise rate.
+// Pass 1 (and the whole standard step when !SUB): the second moment and
+// either its column sums (SUB) or the first moment and the W update with the
+// entrywise rate.
 template <typename T, bool VEC, bool SUB>
 __global__ __launch_bounds__(kBlock) void moments_kernel(T *__restrict__ W, int64_t ldw,
                                                          const T *__restrict__ G, int64_t ldg,
@@ -102,22 +104,21 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(T *__restrict__ W, int6
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
   for (int64_t r = r0; r < r1; ++r) {
-    float g[8], m[8], v[8];
+    float g[8], v[8];
     load8<T, VEC>(G + r * ldg, c0, cols, g);
-    load8<float, VEC>(M + r * ldm, c0, cols, m);
     load8<float, VEC>(V + r * ldm, c0, cols, v);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      m[i] = fmaf(a.b1, m[i], a.omb1 * g[i]);
-      v[i] = fmaf(a.b2, v[i], a.omb2 * (g[i] * g[i]));
-    }
-    store8<float, VEC>(M + r * ldm, c0, cols, m);
+    for (int i = 0; i < 8; ++i) v[i] = fmaf(a.b2, v[i], a.omb2 * (g[i] * g[i]));
     store8<float, VEC>(V + r * ldm, c0, cols, v);
     if constexpr (SUB) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[i] += v[i];
     } else {
-      float w[8];
+      float m[8], w[8];
+      load8<float, VEC>(M + r * ldm, c0, cols, m);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) m[i] = fmaf(a.b1, m[i], a.omb1 * g[i]);
+      store8<float, VEC>(M + r * ldm, c0, cols, m);
       load8<T, VEC>(W + r * ldw, c0, cols, w);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -150,10 +151,12 @@ __global__ __launch_bounds__(kBlock) void alpha_kernel(const float *__restrict__
   alpha[c] = static_cast<float>(1.0 / (sqrt(nu) + eps));
 }
 
-// Pass 3: W <- W - lr alpha_c M^ - wd W with the column's rate.
+// Pass 3: M <- b1 M + (1 - b1) G, then W <- W - lr alpha_c M^ - wd W with
+// the column's rate.
 template <typename T, bool VEC>
 __global__ __launch_bounds__(kBlock) void apply_kernel(T *__restrict__ W, int64_t ldw,
-                                                       const float *__restrict__ M, int64_t ldm,
+                                                       const T *__restrict__ G, int64_t ldg,
+                                                       float *__restrict__ M, int64_t ldm,
                                                        int64_t rows, int64_t cols, AdamArgs a,
                                                        const float *__restrict__ alpha) {
   const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kCols;
@@ -166,11 +169,16 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(T *__restrict__ W, int64_
   for (int i = 0; i < 8; ++i) al[i] *= a.lr * a.inv_bc1;
 #pragma unroll 4
   for (int64_t r = r0; r < r1; ++r) {
-    float m[8], w[8];
+    float g[8], m[8], w[8];
+    load8<T, VEC>(G + r * ldg, c0, cols, g);
     load8<float, VEC>(M + r * ldm, c0, cols, m);
     load8<T, VEC>(W + r * ldw, c0, cols, w);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) w[i] = w[i] - al[i] * m[i] - a.wd * w[i];
+    for (int i = 0; i < 8; ++i) {
+      m[i] = fmaf(a.b1, m[i], a.omb1 * g[i]);
+      w[i] = w[i] - al[i] * m[i] - a.wd * w[i];
+    }
+    store8<float, VEC>(M + r * ldm, c0, cols, m);
     store8<T, VEC>(W + r * ldw, c0, cols, w);
   }
 }
@@ -194,7 +202,7 @@ hipError_t launch_t(void *Wv, int64_t ldw, const void *Gv, int64_t ldg, float *M
                                                        colsum);
   alpha_kernel<<<dim3(static_cast<unsigned>(ceil_div(cols, kBlock))), kBlock, 0, s>>>(
       colsum, grid.y, rows, cols, inv_bc2, eps, alpha);
-  apply_kernel<T, VEC><<<grid, kBlock, 0, s>>>(W, ldw, M, ldm, rows, cols, a, alpha);
+  apply_kernel<T, VEC><<<grid, kBlock, 0, s>>>(W, ldw, G, ldg, M, ldm, rows, cols, a, alpha);
   return hipGetLastError();
 }
 
