@@ -479,6 +479,10 @@ def test_deterministic_bitwise():
 
 @pytest.mark.parametrize("dtype,d,k,widths,pad", [
     ("bf16", 4096, 40, (4096, 14336), 0),      # config 2's Wo and W2 side by side
+    # wide calls (one launch per pass over 16384 or more columns), k from 8 to 64
+    ("bf16", 256, 8, (16384,), 0),
+    ("bf16", 512, 20, (8192, 8192, 2048), 8),  # three segments, strided rows
+    ("bf16", 384, 64, (16384, 256), 0),
     ("bf16", 512, 40, (256, 768, 512), 8),     # strided rows
     ("bf16", 512, 40, (300, 512), 0),          # a width not a multiple of 256: one by one
     ("bf16", 512, 100, (256, 512), 0),         # k > 64: one by one
