@@ -373,20 +373,23 @@ def test_out_of_range_ids_are_clamped_and_flagged(dtype):
 
 
 @pytest.mark.parametrize("pattern", ["one id", "all distinct", "two ids", "zipf"])
-@pytest.mark.parametrize("n,seq", [(512, 64), (500, 50), (1024, 32)])
-def test_compress_token_id_patterns(pattern, n, seq):
+@pytest.mark.parametrize("n,seq,d", [(512, 64, 512), (500, 50, 512), (1024, 32, 512),
+                                     (32768, 4096, 256), (32768, 64, 256), (32769, 32769, 256)])
+def test_compress_token_id_patterns(pattern, n, seq, d):
     """The compress copies each distinct T_fixed row of a workgroup once and
     maps every token to its row: ids that all repeat, never repeat, alternate,
-    or follow Zipf, in position-major (n = batch x seq, batch 8 or 32) and
-    token-major (500 tokens) order."""
-    d, k, vocab = 512, 40, 700
+    or follow Zipf, in position-major (n = batch x seq, batch 8, 32 or 512)
+    and token-major (500 and 32769 tokens) order; at 32768 tokens the
+    workgroups hold 128 tokens (two per lane of the id scan), below that 64."""
+    k = 40
+    vocab = n + 5 if pattern == "all distinct" else 700
     log(f"[id patterns] {pattern} n={n} seq={seq}")
     rng = np.random.default_rng(n + len(pattern))
     U, _ = np.linalg.qr(rng.standard_normal((d, k)))
     E = rng.standard_normal((vocab, d)) * 0.05
     P = rng.standard_normal((seq, d)) * 0.05
     tok = {"one id": np.full(n, 17),
-           "all distinct": rng.permutation(vocab)[:n] if n <= vocab else np.arange(n) % vocab,
+           "all distinct": rng.permutation(vocab)[:n],
            "two ids": np.where(np.arange(n) % 2 == 0, 3, vocab - 1),
            "zipf": np.minimum(rng.zipf(1.1, n), vocab) - 1}[pattern].astype(np.int32)
     pos = (np.arange(n) % seq).astype(np.int32)
