@@ -243,8 +243,8 @@ def traffic_summary(fetch_dir: str, write_dir: str):
 def trace_summary(trace_dir: str, bench_log: str):
     """Per-kernel durations of a ``rocprofv3 --kernel-trace`` run of this
     script, split into the phases main() runs in order: set-up, the warm-up
-    and timed steps, the two back-to-back pair loops, the table build and the
-    projected compress alone.  Only this library's kernels are counted; the
+    and timed steps, the two back-to-back pair loops, the cold pairs, the
+    projected compress alone and the table build.  Only this library's kernels are counted; the
     phases are found from the dispatch order (a step starts at each compress
     launch and has a fixed number of launches)."""
     files = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
@@ -275,17 +275,27 @@ def trace_summary(trace_dir: str, bench_log: str):
     cuts.append(("timed steps, event per op", at, at + K * per_step))
     e = cuts[-1][2]
     e2 = e + 2 * pair
+    e3 = e2 + 2 * max(5, K // 2)  # the cold pairs
+
+    def is_build(i):  # the table build: the compress kernel with the fp32-row epilogue
+        return names[i].startswith("compress_kernel<") and names[i].endswith(", 2>")
+
     proj = OP_KERNELS["compress_projected"][0]
-    tb_end = next((i for i in range(e2, len(rows)) if proj in rows[i]["Kernel_Name"]), None)
-    if tb_end is None or tb_end + K > len(rows):
+    p0 = next((i for i in range(e3, len(rows)) if proj in rows[i]["Kernel_Name"]), None)
+    if p0 is None or p0 + K > len(rows) or not all(is_build(i) for i in range(e3, p0)):
         raise SystemExit("dispatch count does not match the bench's phase layout")
+    b1 = p0 + K
+    while b1 < len(rows) and is_build(b1):
+        b1 += 1
     cuts += [("compress+decompress loop, warm-up", e, e + 6),
              ("compress+decompress loop, timed", e + 6, e + pair),
              ("compress_projected+decompress loop, warm-up", e + pair, e + pair + 6),
              ("compress_projected+decompress loop, timed", e + pair + 6, e2),
-             ("table build", e2, tb_end),
-             ("compress_projected alone", tb_end, tb_end + K)]
-    at = tb_end + K
+             ("compress+decompress, cold (512 MB fill before each pair)", e2, e3),
+             ("table build, warm-up", e3, p0),
+             ("compress_projected alone", p0, p0 + K),
+             ("table build", p0 + K, b1)]
+    at = b1
     grass = [i for i in range(at, len(rows))
              if names[i] in GRASS_KERNELS or names[i].split("<")[0] in GRASS_KERNELS]
     if grass:
@@ -324,6 +334,8 @@ def trace_summary(trace_dir: str, bench_log: str):
                         ev = f"{b['ops'][ops_here[0]]['ms'] * 1e3:.1f}"
                 elif phase == "compress_projected alone":
                     ev = f"{b['codec_pair_projected']['compress_projected_ms'] * 1e3:.1f}"
+                elif phase == "table build":
+                    ev = f"{b['codec_pair_projected']['embed_project_ms'] * 1e3:.1f} (call)"
                 f.write(f"| {phase} | `{n}` | {len(ds)} | {np.mean(ds):.1f} | {np.min(ds):.1f} "
                         f"| {np.max(ds):.1f} | {ev} |\n")
         f.write("\nBench line of the same run (HIP events):\n\n```\n")
@@ -864,16 +876,20 @@ def main():
     cold_ms = float(np.median([a.elapsed_time(b) for a, b in cold]))
     del flush
 
-    # the projected-table compress, back to back over the same buffer rotation
-    # (the tables are rebuilt once, as after a subspace update)
+    # the projected-table compress, back to back over the same buffer rotation,
+    # and the table build (as after a subspace update; two untimed builds
+    # first, so the timed ones reuse the allocator's blocks)
+    for _ in range(2):
+        op("embed_project", 0)
+    torch.cuda.synchronize()
     alt_samples = {"compress_projected": [], "embed_project": []}
-    for i in range(K + 1):
-        nm = "embed_project" if i == 0 else "compress_projected"
-        a, b = mk()
-        a.record(stream)
-        op(nm, args.warmup + i)
-        b.record(stream)
-        alt_samples[nm].append((a, b))
+    for nm in ("compress_projected", "embed_project"):
+        for i in range(K):
+            a, b = mk()
+            a.record(stream)
+            op(nm, args.warmup + i)
+            b.record(stream)
+            alt_samples[nm].append((a, b))
     torch.cuda.synchronize()
     alt_ms = {nm: float(np.mean([a.elapsed_time(b) for a, b in v])) for nm, v in alt_samples.items()}
 
