@@ -166,66 +166,27 @@ __global__ __launch_bounds__(256) void reset_kernel(double *__restrict__ state, 
 // ---------------------------------------------------------------------------
 // accumulate, MFMA path
 // ---------------------------------------------------------------------------
-// One thread per (operand part, token step s, column tile t, lane) writes the
-// 8 bf16 F[32 s + 8 g + e, 16 t + n] of the kfrag layout.  Column c of
-// operand 1 of 1 is C_hi[:, c] for c < k and C_lo[:, c - k] for k <= c < 2k;
-// of 2 operands, part 0 is C_hi and part 1 C_lo.  Zero past the columns and
-// past row N.
-__global__ __launch_bounds__(256) void frag_kernel(const float *__restrict__ c32, int64_t kp,
-                                                   int64_t N, int64_t k, int nparts, int ktb,
-                                                   int64_t npad, bf16_t *__restrict__ frag) {
-  const int64_t slot = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  const int64_t per_part = (npad / 32) * ktb * 64;
-  if (slot >= nparts * per_part) return;
-  const int p = static_cast<int>(slot / per_part);
-  const int64_t rem = slot - p * per_part;
-  const int64_t blk = rem >> 6;
-  const int lane = static_cast<int>(rem & 63);
-  const int64_t s = blk / ktb;
-  const int64_t t = blk - s * ktb;
-  const int g = lane >> 4, n = lane & 15;
-  const int64_t c2 = 16 * t + n;
-  bool lo;
-  int64_t col;
-  if (nparts == 1) {
-    lo = c2 >= k;
-    col = lo ? c2 - k : c2;
-  } else {
-    lo = p == 1;
-    col = c2;
-  }
-  const bool cvalid = col < k;
-  uint32_t w[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    bf16_t h[2];
-#pragma unroll
-    for (int e2 = 0; e2 < 2; ++e2) {
-      const int64_t row = 32 * s + 8 * g + 2 * q + e2;
-      h[e2] = bf16_t(0);
-      if (cvalid && row < N) {
-        const float x = c32[row * kp + col];
-        const bf16_t hi = from_f32<bf16_t>(x);
-        h[e2] = lo ? from_f32<bf16_t>(x - to_f32(hi)) : hi;
-      }
-    }
-    w[q] = static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
-  }
-  *reinterpret_cast<u32x4 *>(frag + slot * 8) = u32x4{w[0], w[1], w[2], w[3]};
-}
-
 // Loss terms |g|^2 - |c|^2 + c D c^T of 64 rows per block, summed: the
 // block's coefficient rows are staged in LDS with coalesced loads (row stride
 // 16 KT + 1 words, so per-lane row reads hit distinct banks); wave w takes the
 // coefficient indices a = w, w + 4, ... of every row (lane = row), with D's row
 // a read by uniform loads (D is padded to 16 KT columns, and so are the rows:
 // the padding is zero on both sides); the four waves' sums meet in LDS in a
-// fixed order.
+// fixed order.  Blocks past the nlblk that hold rows write no loss term.
+//
+// With frag, the same staged rows also give the token contraction's operand
+// F in the kfrag layout: per (operand part p, token step s, column tile t,
+// lane 16 g + n) the 8 bf16 F[32 s + 8 g + e, 16 t + n].  Column c of operand
+// 1 of 1 is C_hi[:, c] for c < k and C_lo[:, c - k] for k <= c < 2k; of 2
+// operands, part 0 is C_hi and part 1 C_lo.  Zero past the columns and past
+// row N (the grid then covers all npad rows).
 template <int KT>
 __global__ __launch_bounds__(256) void loss_kernel(const float *__restrict__ c32,
                                                    const double *__restrict__ gsq,
                                                    const double *__restrict__ dgram, int64_t N,
-                                                   int64_t k, double *__restrict__ part) {
+                                                   int64_t k, double *__restrict__ part,
+                                                   int64_t nlblk, bf16_t *__restrict__ frag,
+                                                   int nparts, int ktb, int64_t npad) {
   constexpr int KP = 16 * KT, LDL = KP + 1;
   __shared__ float cs[64 * LDL];
   __shared__ double red[256];
@@ -263,24 +224,70 @@ __global__ __launch_bounds__(256) void loss_kernel(const float *__restrict__ c32
     l = gsq[r0 + lane] + (((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane]);
   __syncthreads();
   const double tot = block_sum256(l, red);
-  if (threadIdx.x == 0) part[blockIdx.x] = tot;
+  if (threadIdx.x == 0 && blockIdx.x < nlblk) part[blockIdx.x] = tot;
+  if (!frag) return;
+  const int64_t per_part = (npad / 32) * ktb * 64;
+  const int nsl = nparts * 2 * ktb * 64;  // the block's two token steps
+  for (int sl = threadIdx.x; sl < nsl; sl += 256) {
+    const int p = sl / (2 * ktb * 64);
+    const int rem = sl - p * (2 * ktb * 64);
+    const int sb = rem / (ktb * 64);
+    const int t = (rem / 64) % ktb;
+    const int l2 = rem & 63;
+    const int g = l2 >> 4, n = l2 & 15;
+    const int64_t c2 = 16 * t + n;
+    bool lo;
+    int64_t col;
+    if (nparts == 1) {
+      lo = c2 >= k;
+      col = lo ? c2 - k : c2;
+    } else {
+      lo = p == 1;
+      col = c2;
+    }
+    const bool cvalid = col < k;
+    uint32_t wd[4];
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      bf16_t h[2];
+#pragma unroll
+      for (int e2 = 0; e2 < 2; ++e2) {
+        const int lr = 32 * sb + 8 * g + 2 * qq + e2;  // row within the block
+        h[e2] = bf16_t(0);
+        if (cvalid && lr < nr) {
+          const float x = cs[lr * LDL + col];
+          const bf16_t hi = from_f32<bf16_t>(x);
+          h[e2] = lo ? from_f32<bf16_t>(x - to_f32(hi)) : hi;
+        }
+      }
+      wd[qq] = static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
+    }
+    const int64_t s = r0 / 32 + sb;
+    const int64_t slot = p * per_part + (s * ktb + t) * 64 + l2;
+    *reinterpret_cast<u32x4 *>(frag + slot * 8) = u32x4{wd[0], wd[1], wd[2], wd[3]};
+  }
 }
 
+// The loss terms, and with frag the token contraction's operand (npad a
+// multiple of 64: the grid then covers every operand row).
 hipError_t launch_loss(int kt, const float *c32, const double *gsq, const double *dgram,
-                       int64_t N, int64_t k, double *part, int64_t nlblk, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(ceil_div(N, 64)));
-  (void)nlblk;
+                       int64_t N, int64_t k, double *part, int64_t nlblk, bf16_t *frag,
+                       int nparts, int ktb, int64_t npad, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(frag ? npad / 64 : nlblk));
+#define SN_LOSS(KT) \
+  loss_kernel<KT><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part, nlblk, frag, nparts, ktb, npad)
   switch (kt) {
-    case 1: loss_kernel<1><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 2: loss_kernel<2><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 3: loss_kernel<3><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 4: loss_kernel<4><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 5: loss_kernel<5><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 6: loss_kernel<6><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 7: loss_kernel<7><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
-    case 8: loss_kernel<8><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part); break;
+    case 1: SN_LOSS(1); break;
+    case 2: SN_LOSS(2); break;
+    case 3: SN_LOSS(3); break;
+    case 4: SN_LOSS(4); break;
+    case 5: SN_LOSS(5); break;
+    case 6: SN_LOSS(6); break;
+    case 7: SN_LOSS(7); break;
+    case 8: SN_LOSS(8); break;
     default: return hipErrorNotSupported;
   }
+#undef SN_LOSS
   return hipGetLastError();
 }
 
@@ -587,16 +594,12 @@ hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, cons
     go.gsq = reinterpret_cast<double *>(w + P.off_gsq);
     hipError_t e = launch_grass_compress_mfma(L, packed, G, N, ldg, go, Cwire, ldc, s);
     if (e != hipSuccess) return e;
-    e = launch_loss(P.kt, go.c32, go.gsq, reinterpret_cast<const double *>(base + L.off_gram),
-                    N, L.k, part, P.nlblk, s);
-    if (e != hipSuccess) return e;
     bf16_t *frag = reinterpret_cast<bf16_t *>(w + P.off_frag);
+    e = launch_loss(P.kt, go.c32, go.gsq, reinterpret_cast<const double *>(base + L.off_gram),
+                    N, L.k, part, P.nlblk, with_su ? frag : nullptr, P.nparts, P.ktb, P.npad, s);
+    if (e != hipSuccess) return e;
     float *tp = reinterpret_cast<float *>(w + P.off_tp);
     if (with_su) {
-      const int64_t nfrag = ceil_div(P.nparts * (P.npad / 32) * P.ktb * 64, 256);
-      frag_kernel<<<dim3(static_cast<unsigned>(nfrag)), 256, 0, s>>>(go.c32, go.kp, N, L.k,
-                                                                     P.nparts, P.ktb, P.npad,
-                                                                     frag);
       const int64_t per_part = static_cast<int64_t>(P.npad / 32) * P.ktb * 512;
       for (int p = 0; p < P.nparts; ++p) {
         e = launch_grass_tokens_mfma(frag + p * per_part, P.ktb, P.npad, G, N, ldg, L.d, P.rows,
