@@ -108,8 +108,14 @@ template <> struct P1Vec<4> { typedef u32x2 T; };
 // CLAMP: rows at or past nrows read row nrows - 1 instead (the caller's
 // operand is zero there), for a reduction length that is not a multiple of
 // the split size (the subspace update's contraction over tokens).
+// Row steps in flight per wave: the weight projection at k <= 48 runs two
+// waves per SIMD with a 2-deep ring (same bytes in flight per CU, twice the
+// waves to issue them); otherwise one wave per SIMD with a 4-deep ring.
+template <int KT, bool CLAMP>
+constexpr bool p1_two_waves() { return !CLAMP && KT <= 3; }
+
 template <int KT, bool CLAMP = false, int CW = p1_cw<KT>()>
-__global__ __launch_bounds__(kBlock) void project_pass1_kernel(
+__global__ __launch_bounds__(kBlock, (p1_two_waves<KT, CLAMP>() ? 2 : 1)) void project_pass1_kernel(
     const bf16_t *__restrict__ kfrag, int64_t d, ColSegs ws, int64_t rows_per_split,
     int64_t m_pad, float *__restrict__ Tp, int64_t nrows = 0) {
   constexpr int W32 = CW / 2;  // 32-bit words per lane and row
@@ -182,10 +188,10 @@ __global__ __launch_bounds__(kBlock) void project_pass1_kernel(
     }
   };
 
-  // PD-deep ring of row steps in flight (memory latency under load is long
-  // and there is one wave per SIMD): step s + PD is loaded as soon as step s
-  // has been consumed; past the end the last step is reloaded.
-  constexpr int PD = 4;
+  // PD-deep ring of row steps in flight (memory latency under load is long):
+  // step s + PD is loaded as soon as step s has been consumed; past the end
+  // the last step is reloaded.
+  constexpr int PD = p1_two_waves<KT, CLAMP>() ? 2 : 4;
   if (s0 < s1) {
     vec v[PD][8];
     u32x4 a[PD][KT];
