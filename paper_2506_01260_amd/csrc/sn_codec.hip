@@ -42,6 +42,8 @@
 //
 // stream_compress_kernel (X U with no gathered rows) is described at its
 // definition.
+#include <atomic>
+
 #include "sn_mfma_common.h"
 
 namespace sn {
@@ -656,19 +658,20 @@ bool pm_tiling_ok(int64_t N, const IdArgs &ids, int bp, int nw) {
   return batch % bp == 0 && ids.seq_len % (16 / bp) == 0 && (N / 16) % nw == 0;
 }
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (cached per device; concurrent first
+// calls store the same value).
 int device_cus() {
-  static int cached[64] = {};
+  static std::atomic<int> cached[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int c = 0;
+  int c = cached[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
     if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         c <= 0)
       c = 256;
-    cached[dev] = c;
+    cached[dev].store(c, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return c;
 }
 
 // Compute waves of a launch over N tokens: 8 where the stage buffers allow
