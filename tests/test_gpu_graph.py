@@ -25,7 +25,8 @@ def _bits(t: torch.Tensor) -> np.ndarray:
         t.view(torch.int32).cpu().numpy()
 
 
-@pytest.mark.parametrize("d,k,n,m", [(1024, 40, 4096, 2048), (512, 20, 1000, 384)])
+@pytest.mark.parametrize("d,k,n,m", [(1024, 40, 4096, 2048), (512, 20, 1000, 384),
+                                     (256, 40, 32768, 256)])  # 128-token compress workgroups
 def test_graph_replays_match_eager(d, k, n, m):
     log(f"[graph] d={d} k={k} n={n} m={m}")
     g = torch.Generator(device="cuda")
