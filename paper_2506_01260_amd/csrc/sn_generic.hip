@@ -107,14 +107,15 @@ __global__ __launch_bounds__(256) void pack_uu_kernel(const bf16_t *__restrict__
 // U^T U - I from the float32 section (exact copies of the stored U), as a
 // kp x kp matrix (kp = 16 ceil(k/16) <= 256, zero outside k x k).  One
 // workgroup per row a; thread (h, b) sums U[r, a] U[r, b] in float64 over the
-// rows r = h mod H (H = 256 / kp row phases, reads coalesced along b), and the
-// H partial sums are added in a fixed order.
-__global__ __launch_bounds__(256) void pack_gram_kernel(const float *__restrict__ U32, int64_t d,
-                                                        int64_t k, int64_t kp,
-                                                        double *__restrict__ out) {
-  __shared__ double red[256];
+// rows r = h mod H (H = 1024 / kp row phases, reads coalesced along b), and
+// the H partial sums are added in a fixed order.
+constexpr int kGramThreads = 1024;
+__global__ __launch_bounds__(kGramThreads) void pack_gram_kernel(const float *__restrict__ U32,
+                                                                 int64_t d, int64_t k, int64_t kp,
+                                                                 double *__restrict__ out) {
+  __shared__ double red[kGramThreads];
   const int64_t a = blockIdx.x;
-  const int H = static_cast<int>(256 / kp);
+  const int H = static_cast<int>(kGramThreads / kp);
   const int h = static_cast<int>(threadIdx.x / kp), b = static_cast<int>(threadIdx.x % kp);
   double acc = 0.0;
   if (a < k && h < H && b < k) {
@@ -159,7 +160,7 @@ hipError_t launch_pack(const PackLayout &L, const void *U, int64_t ldu, void *pa
     }
   }
   const int64_t kp = 16 * L.kt;
-  pack_gram_kernel<<<dim3(static_cast<unsigned>(kp)), 256, 0, s>>>(
+  pack_gram_kernel<<<dim3(static_cast<unsigned>(kp)), kGramThreads, 0, s>>>(
       reinterpret_cast<const float *>(base + L.off_f32), L.d, L.k, kp,
       reinterpret_cast<double *>(base + L.off_gram));
   return hipGetLastError();
