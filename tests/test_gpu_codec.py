@@ -404,6 +404,34 @@ def test_compress_token_id_patterns(pattern, n, seq, d):
     assert_parity(host(C), ref, "bf16", f"compress, {pattern}")
 
 
+@pytest.mark.parametrize("tables", ["E only", "P only"])
+def test_compress_one_table_128_token_workgroups(tables):
+    """One gathered table at 32768 tokens (the 128-token workgroups): T_fixed
+    alone (distinct-row copies, no positional rows) or P alone
+    (position-major positional rows, no T_fixed)."""
+    d, k, n, seq, vocab = 256, 40, 32768, 4096, 2000
+    log(f"[one table] {tables} n={n}")
+    rng = np.random.default_rng(77 if tables == "E only" else 78)
+    U, _ = np.linalg.qr(rng.standard_normal((d, k)))
+    E = rng.standard_normal((vocab, d)) * 0.05
+    P = rng.standard_normal((seq, d)) * 0.05
+    tok = (np.minimum(rng.zipf(1.1, n), vocab) - 1).astype(np.int32)
+    pos = (np.arange(n) % seq).astype(np.int32)
+    use_e, use_p = tables == "E only", tables == "P only"
+    X = (E[tok] if use_e else 0) + (P[pos] if use_p else 0) + rng.standard_normal((n, d)) * 0.05
+    st = {nm: synth.store(a, "bf16") for nm, a in dict(U=U, E=E, P=P, X=X).items()}
+    f64 = {nm: oracle.decode_bf16(a) for nm, a in st.items()}
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    kw = dict(tok=ids(tok), E=dev(st["E"], "bf16")) if use_e else dict(P=dev(st["P"], "bf16"),
+                                                                      seq_len=seq)
+    C = sn.sn_compress(basis, dev(st["X"], "bf16"), **kw)
+    ref = oracle.round_to(oracle.compress(f64["X"], f64["U"], tok if use_e else None,
+                                          f64["E"] if use_e else None,
+                                          f64["P"] if use_p else None,
+                                          seq_len=seq if use_p else None), "bf16")
+    assert_parity(host(C), ref, "bf16", f"compress, {tables}")
+
+
 def test_bit_exact_gather_and_subtract():
     """C = 0 decompresses to exactly E[tok] + P[pos]; X = E[tok] + P[pos]
     compresses to exactly 0 (values on a grid where every sum is exact)."""
