@@ -9,8 +9,8 @@
 // Without tables this is the gradient compress of Sec. 4.4.
 //
 // compress_kernel (one workgroup = NW compute waves + 3 producer waves, 16 NW
-// tokens; NW = 8 where four stage buffers still fit in LDS and the launch
-// has a workgroup for every CU, else 4):
+// tokens; NW = 8 where three stage buffers of that width fit in LDS and the
+// launch has a workgroup for every CU, else 4):
 //
 // * Three producer waves copy, for each stage of 64 columns of d, everything
 //   the compute waves need into one of NB LDS buffers with direct-to-LDS
@@ -128,13 +128,13 @@ struct CGeo {
   static_assert(nb >= 3, "at least two stages in flight");
 };
 
-// Compute waves per workgroup: 8 while four stage buffers of that width fit
-// in LDS, else 4.
+// Compute waves per workgroup: 8 while three stage buffers of that width fit
+// in LDS (four at k <= 48 with both tables, three above), else 4.
 template <int KT, bool HE, bool HP, int BP>
 constexpr int nw_of() {
   constexpr int rows = 128 * (HE ? 2 : 1) + (HP ? p_rows<8, BP>() : 0);  // X, T_fixed, P rows
   constexpr int units = rows * kPieces + (kStageCols / 32) * KT * 64;
-  return kLdsBytes / (units * 16) >= 4 ? 8 : 4;
+  return kLdsBytes / (units * 16) >= 3 ? 8 : 4;
 }
 
 // ---------------------------------------------------------------------------
