@@ -62,7 +62,7 @@ OP_KERNELS = {
 # kernels that only the subspace update launches
 GRASS_KERNELS = ["loss_kernel", "finish_kernel", "gram_partial_kernel", "gram_reduce_kernel",
                  "moments_kernel", "alpha_kernel", "apply_kernel", "gather_rows_kernel",
-                 "zero_kernel", "hist_kernel", "block_prefix_kernel", "tile_scan_kernel",
+                 "hist_kernel", "block_prefix_kernel", "tile_scan_kernel",
                  "tiles_scan_kernel", "tile_write_kernel", "place_kernel",
                  "chunk_sum_kernel", "seg_sum_kernel",
                  "update_kernel", "chol_kernel", "tri_apply_kernel", "reset_kernel",

@@ -120,18 +120,18 @@ __device__ __forceinline__ int clamp_tok(const int32_t *tok, int64_t i, int64_t 
   return static_cast<int>(v);
 }
 
-__global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i < n) p[i] = 0;
-}
-
-// cnt[b][v] = number of tokens of block b (1024 tokens each) with id v
+// cnt[b][v] = number of tokens of block b (1024 tokens each) with id v; the
+// block clears its own row first (the barrier orders the clearing stores
+// before the block's increments)
 __global__ __launch_bounds__(kSortThreads) void hist_kernel(const int32_t *__restrict__ tok,
                                                             int64_t N, int64_t vocab,
                                                             int32_t *err_flag,
                                                             int32_t *__restrict__ cnt) {
+  int32_t *row = cnt + static_cast<int64_t>(blockIdx.x) * vocab;
+  for (int64_t v = threadIdx.x; v < vocab; v += kSortThreads) row[v] = 0;
+  __syncthreads();
   const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
-  if (i < N) atomicAdd(&cnt[static_cast<int64_t>(blockIdx.x) * vocab + clamp_tok(tok, i, vocab, err_flag)], 1);
+  if (i < N) atomicAdd(&row[clamp_tok(tok, i, vocab, err_flag)], 1);
 }
 
 // per id v: cnt[b][v] <- tokens of id v in the blocks before b; tot[v] <- all of them
@@ -373,8 +373,6 @@ hipError_t launch_embed_backward(const PackLayout &L, const void *packed, const 
                      : launch_table_project_generic(L, packed, dX0, N, ldg, c32, P.kp, s);
   if (e != hipSuccess) return e;
   auto I = [&](size_t off) { return reinterpret_cast<int32_t *>(w + off); };
-  const int64_t nc = P.nblk * vocab;
-  zero_kernel<<<dim3(static_cast<unsigned>(ceil_div(nc, 256))), 256, 0, s>>>(I(P.off_cnt), nc);
   hist_kernel<<<dim3(static_cast<unsigned>(P.nblk)), kSortThreads, 0, s>>>(tok, N, vocab,
                                                                            err_flag, I(P.off_cnt));
   block_prefix_kernel<<<dim3(static_cast<unsigned>(ceil_div(vocab, 256))), 256, 0, s>>>(
