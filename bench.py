@@ -220,13 +220,13 @@ def traffic_summary(fetch_dir: str, write_dir: str):
     md = TRAFFIC_FILE[:-5] + ".md"
     with open(md, "w") as f:
         f.write("# HBM traffic per launch: codec step at d=4096, k=40, N=32768 (bf16)\n\n")
-        f.write("Commands (repository root on the GPU box as `$R`; `cd /tmp && export "
+        f.write("Commands (repository root `$R`, output directory `$OUT`; `cd /tmp && export "
                 "TMPDIR=/tmp` first), one counter per run:\n\n```\n"
-                "rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/pmc_fetch -o f --output-format csv "
+                "rocprofv3 --pmc FETCH_SIZE -d $OUT/pmc_fetch -o f --output-format csv "
                 "-- python3 $R/bench.py --profile-pass\n"
-                "rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/pmc_write -o w --output-format csv "
+                "rocprofv3 --pmc WRITE_SIZE -d $OUT/pmc_write -o w --output-format csv "
                 "-- python3 $R/bench.py --profile-pass\n"
-                "python3 bench.py --traffic-summary gpurun_out/pmc_fetch gpurun_out/pmc_write\n```\n\n")
+                "python3 $R/bench.py --traffic-summary $OUT/pmc_fetch $OUT/pmc_write\n```\n\n")
         f.write(f"Scale: a streaming kernel (`y = 1.0 * x`, fp32) that reads and writes "
                 f"{CALIB_BYTES} bytes (torch `mul` fp32 elementwise kernel) "
                 f"reads {cf:.0f} KiB and writes {cw:.0f} KiB per dispatch; counters are "
@@ -307,12 +307,12 @@ def trace_summary(trace_dir: str, bench_log: str):
     out = os.path.join(ROOT, "profiles", "codec_step_d4096_k40_kernel_stats.md")
     with open(out, "w") as f:
         f.write("# Kernel durations: codec step at d=4096, k=40, N=32768 (bf16)\n\n")
-        f.write("Commands (repository root on the GPU box as `$R`; `cd /tmp && export "
+        f.write("Commands (repository root `$R`, output directory `$OUT`; `cd /tmp && export "
                 "TMPDIR=/tmp` first):\n\n```\n"
-                f"rocprofv3 --kernel-trace --stats -d $R/gpurun_out/prof_step -o step "
+                f"rocprofv3 --kernel-trace --stats -d $OUT/prof_step -o step "
                 f"--output-format csv -- python3 $R/bench.py --steps {K} --warmup {W} "
-                f"--no-cpu-baseline > $R/gpurun_out/prof_step.log\n"
-                "python3 bench.py --trace-summary gpurun_out/prof_step gpurun_out/prof_step.log\n"
+                f"--no-cpu-baseline > $OUT/prof_step.log\n"
+                "python3 $R/bench.py --trace-summary $OUT/prof_step $OUT/prof_step.log\n"
                 "```\n\n")
         f.write(f"Source hash `{source_hash()}`. Durations are rocprofv3's kernel begin/end "
                 f"timestamps; the bench's own figures (HIP events around each launch on the "
