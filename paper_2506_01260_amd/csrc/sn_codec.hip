@@ -382,6 +382,10 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
       lds_barrier();
       if (s + NB - 1 < nst) issue(s + NB - 1);
     }
+    if constexpr (HP && PM) {  // the compute waves' exchange of the positional products
+      lds_barrier();
+      lds_barrier();
+    }
     return;
   }
 
@@ -399,6 +403,18 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
 #pragma unroll
   for (int t = 0; t < KT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   double sq = 0.0;  // kEpiGrass: sum of squares of the lane's elements of its row
+
+  // Position-major tiles: the workgroup has only PR positional rows, so their
+  // products (-P) U are formed once per row rather than once per token: the
+  // jobs (P tile pt of 16 rows, column tile t) are dealt to the compute waves
+  // (at most two each), and after the last stage every token adds its row's
+  // product through LDS.
+  constexpr bool kPT = HP && PM;
+  constexpr int PR = p_rows<NW, BP>();
+  constexpr int NJOB = ((PR + 15) / 16) * KT;
+  constexpr int JPW = (NJOB + NW - 1) / NW;
+  static_assert(!kPT || JPW <= 2, "at most two positional jobs per wave");
+  f32x4 pacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 
   for (int s = 0; s < nst; ++s) {
     lds_barrier();  // stage s is in buffer s % NB
@@ -421,15 +437,46 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
       }
       u32x4 be, bpv;
       if (HE) be = neg8(b[G::e_off + slot(erow, pc)]);
-      if (HP) bpv = neg8(b[G::p_off + slot(prow, pc)]);
+      if (HP && !kPT) bpv = neg8(b[G::p_off + slot(prow, pc)]);
 #pragma unroll
       for (int t = 0; t < KT; ++t) {
         const u32x4 a = b[G::u_off + (j * KT + t) * 64 + lane];
         acc[t] = mfma(a, bx, acc[t]);
-        if (HP) acc[t] = mfma(a, bpv, acc[t]);
+        if (HP && !kPT) acc[t] = mfma(a, bpv, acc[t]);
         if (HE) acc[t] = mfma(a, be, acc[t]);
       }
+      if constexpr (kPT) {
+#pragma unroll
+        for (int jj = 0; jj < JPW; ++jj) {
+          const int job = wave + jj * NW;  // wave-uniform
+          if (job < NJOB) {
+            const int pt = job / KT, t = job % KT;
+            int r = 16 * pt + n;
+            r = r < PR ? r : PR - 1;  // rows past the workgroup's are not used
+            const u32x4 bp = neg8(b[G::p_off + slot(r, pc)]);
+            pacc[jj] = mfma(b[G::u_off + (j * KT + t) * 64 + lane], bp, pacc[jj]);
+          }
+        }
+      }
     }
+  }
+  if constexpr (kPT) {
+    lds_barrier();  // every wave has read the last stage
+    float *pu = reinterpret_cast<float *>(lds);  // PR x 16 KT floats in buffer 0
+#pragma unroll
+    for (int jj = 0; jj < JPW; ++jj) {
+      const int job = wave + jj * NW;
+      if (job < NJOB) {
+        const int pt = job / KT, t = job % KT;
+        const int r = 16 * pt + n;
+        // lane (g, n) holds (-P U)[row r][16 t + 4 g .. + 3]
+        if (r < PR) *reinterpret_cast<f32x4 *>(pu + r * (16 * KT) + 16 * t + 4 * g) = pacc[jj];
+      }
+    }
+    lds_barrier();
+#pragma unroll
+    for (int t = 0; t < KT; ++t)
+      acc[t] += *reinterpret_cast<const f32x4 *>(pu + prow * (16 * KT) + 16 * t + 4 * g);
   }
 
   // epilogue: lane (g, n) holds C[token, 16 t + 4 g .. +3]
