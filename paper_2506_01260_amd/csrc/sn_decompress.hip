@@ -211,17 +211,19 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
 
   auto load_tile = [&](DTile<KS> &dt, int j) {
     const unsigned T = tile_of(j);
-    load_coeffs<KS, CM>(dt, token(T, n), C, ldc, k, g);
+    const int jc = j < nt ? j : nt - 1;
+    const int t0 = dtile_token0(tm, T);  // the tile's first token, once per tile
+    auto tok_of = [&](int r) { return t0 + r < tm.N ? t0 + r : tm.N - 1; };
+    load_coeffs<KS, CM>(dt, tok_of(n), C, ldc, k, g);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = 4 * i + q;
-      const int t = token(T, r);
       if constexpr (kIds) {
-        const int2 v = sm.idl[wave][j < nt ? j : nt - 1][r];
+        const int2 v = sm.idl[wave][jc][r];
         if (HE) dt.er[i] = static_cast<int>(clamp_flag(v.x, ids.vocab, 1, bad));
         if (HP) dt.pr[i] = static_cast<int>(clamp_flag(v.y, ids.n_pos, 2, bad));
       }
-      dt.xr[i] = t;
+      dt.xr[i] = tok_of(r);
     }
   };
   const bf16_t *Eb = static_cast<const bf16_t *>(ids.E) + col_r;
