@@ -170,7 +170,9 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   };
 
   // Stage the ids of all the wave's tiles in LDS up front (fixed trip count,
-  // clamped tiles: all loads are in flight before the first wait).
+  // clamped tiles: all loads are in flight before the first wait), each id
+  // already clamped into its table (out-of-range ids set a flag bit).
+  int bad = 0;
   if constexpr (kIds) {
     if (nt > 0) {
     int2 v[kMaxWaveTiles / 4];
@@ -190,6 +192,11 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
       }
     }
 #pragma unroll
+    for (int i = 0; i < kMaxWaveTiles / 4; ++i) {
+      if (HE) v[i].x = static_cast<int>(clamp_flag(v[i].x, ids.vocab, 1, bad));
+      if (HP) v[i].y = static_cast<int>(clamp_flag(v[i].y, ids.n_pos, 2, bad));
+    }
+#pragma unroll
     for (int i = 0; i < kMaxWaveTiles / 4; ++i) sm.idl[wave][4 * i + g][n] = v[i];
     }
   }
@@ -205,9 +212,11 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   // the column segment of X that holds this block (blocks never straddle two)
   int sg = 0;
   while (sg + 1 < xs.n && static_cast<int64_t>(cb) * kDCols >= xs.c0[sg + 1]) ++sg;
-  const int64_t ldx = xs.ld[sg];
+  // Row addresses are base + row x row-bytes with both factors below 2^32
+  // (the launch checks the leading dimensions): one 32 x 32 -> 64-bit
+  // multiply-add per row, no 64-bit products.
+  const uint32_t ldx_b = static_cast<uint32_t>(xs.ld[sg] * 2);
   f32x4 *otw = sm.ot[wave];
-  int bad = 0;
 
   auto load_tile = [&](DTile<KS> &dt, int j) {
     const unsigned T = tile_of(j);
@@ -219,19 +228,22 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     for (int i = 0; i < 4; ++i) {
       const int r = 4 * i + q;
       if constexpr (kIds) {
-        const int2 v = sm.idl[wave][jc][r];
-        if (HE) dt.er[i] = static_cast<int>(clamp_flag(v.x, ids.vocab, 1, bad));
-        if (HP) dt.pr[i] = static_cast<int>(clamp_flag(v.y, ids.n_pos, 2, bad));
+        const int2 v = sm.idl[wave][jc][r];  // clamped when staged
+        if (HE) dt.er[i] = v.x;
+        if (HP) dt.pr[i] = v.y;
       }
       dt.xr[i] = tok_of(r);
     }
   };
-  const bf16_t *Eb = static_cast<const bf16_t *>(ids.E) + col_r;
-  const bf16_t *Pb = static_cast<const bf16_t *>(ids.P) + col_r;
-  bf16_t *Xb = static_cast<bf16_t *>(xs.base[sg]) + (col_r - xs.c0[sg]);
-  // The P values are reloaded only when the tile's positions change: in
-  // position-major order a wave's run of tiles holds `batch` tiles with the
-  // same 16 positions in a row, and slot c of the ring keeps chunk c.
+  const char *Eb = reinterpret_cast<const char *>(static_cast<const bf16_t *>(ids.E) + col_r);
+  const char *Pb = reinterpret_cast<const char *>(static_cast<const bf16_t *>(ids.P) + col_r);
+  char *Xb = reinterpret_cast<char *>(static_cast<bf16_t *>(xs.base[sg]) + (col_r - xs.c0[sg]));
+  const uint32_t lde_b = static_cast<uint32_t>(ids.lde * 2);
+  const uint32_t ldp_b = static_cast<uint32_t>(ids.ldp * 2);
+  auto row_at = [](const char *base, int row, uint32_t ld_b) {
+    return reinterpret_cast<const bf16_t *>(
+        base + static_cast<uint64_t>(static_cast<uint32_t>(row)) * ld_b);
+  };
   // T_fixed values are loaded a whole tile ahead (double buffer).  P values
   // are reloaded only when the tile's positions change: in position-major
   // order a wave's run of tiles holds `batch` tiles with the same 16
@@ -242,12 +254,12 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     for (int c = 0; c < kNC; ++c)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        er.v[c][i] = ld16(Eb + static_cast<int64_t>(dt.er[i]) * ids.lde + 128 * c);
+        er.v[c][i] = ld16(row_at(Eb, dt.er[i], lde_b) + 128 * c);
   };
   auto load_p = [&](PRows &pr, const DTile<KS> &dt, int c) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      pr.v[i] = ld16(Pb + static_cast<int64_t>(dt.pr[i]) * ids.ldp + 128 * c);
+      pr.v[i] = ld16(row_at(Pb, dt.pr[i], ldp_b) + 128 * c);
   };
   // whether tile j has other positions than tile j - 1 (always, unless position-major)
   auto new_pos = [&](int j) {
@@ -288,7 +300,7 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
       __builtin_nontemporal_store(
           u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
                 pack_bf16x2(o[6], o[7])},
-          reinterpret_cast<u32x4 *>(Xb + static_cast<int64_t>(dt.xr[i]) * ldx + 128 * c));
+          reinterpret_cast<u32x4 *>(const_cast<bf16_t *>(row_at(Xb, dt.xr[i], ldx_b)) + 128 * c));
     }
   };
 
@@ -380,12 +392,17 @@ void launch_dcb_ks(const bf16_t *rf, const PackLayout &L, const void *C, int64_t
     launch_dcb_t<KS, 2>(rf, L, C, ldc, tm, ids, X, s);
 }
 
-bool table_ok(const void *T, int64_t ld) { return !T || (aligned16(T) && ld % 8 == 0); }
+// Leading dimensions below 2^31 elements keep row x row-bytes products in
+// 32-bit operands (the kernel's row addressing).
+constexpr int64_t kMaxLd = int64_t{1} << 31;
+bool table_ok(const void *T, int64_t ld) {
+  return !T || (aligned16(T) && ld % 8 == 0 && ld < kMaxLd);
+}
 
 }  // namespace
 
 bool decompress_mfma_ok(const PackLayout &L, void *X, int64_t ldx, const IdArgs &ids) {
-  return L.mfma && L.d % kDCols == 0 && aligned16(X) && ldx % 8 == 0 &&
+  return L.mfma && L.d % kDCols == 0 && aligned16(X) && ldx % 8 == 0 && ldx < kMaxLd &&
          table_ok(ids.E, ids.lde) && table_ok(ids.P, ids.ldp);
 }
 
@@ -398,6 +415,9 @@ hipError_t launch_decompress_mfma(const PackLayout &L, const void *packed, const
 hipError_t launch_decompress_mfma_segs(const PackLayout &L, const void *packed, const void *C,
                                        int64_t N, int64_t ldc, const IdArgs &ids,
                                        const ColSegs &X, hipStream_t s) {
+  for (int i = 0; i < X.n; ++i)
+    if (X.ld[i] % 8 != 0 || X.ld[i] >= kMaxLd) return hipErrorNotSupported;
+  if (!table_ok(ids.E, ids.lde) || !table_ok(ids.P, ids.ldp)) return hipErrorNotSupported;
   const bf16_t *rf =
       reinterpret_cast<const bf16_t *>(static_cast<const char *>(packed) + L.off_rfrag);
   // how the coefficient rows may be read: 16-byte chunks, 4-byte pairs, or bf16 by bf16
