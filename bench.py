@@ -262,7 +262,7 @@ def trace_summary(trace_dir: str, bench_log: str):
     comp = _short(next(r["Kernel_Name"] for r in rows if OP_KERNELS["compress"][0] in r["Kernel_Name"]))
     starts = [i for i, n in enumerate(names) if n == comp]
     s0, per_step = starts[0], starts[1] - starts[0]
-    pair = 2 * (3 + K)
+    pair = 2 * (3 + 3 * K)  # 3 warm-up pairs, then three timed runs of K pairs
     R = b["config"].get("rotate_buffers", 3)
     cuts = [("set-up", 0, s0),
             ("warm-up steps", s0, s0 + W * per_step),
@@ -347,7 +347,8 @@ def trace_summary(trace_dir: str, bench_log: str):
 
 def _pair_times(sn, torch, basis, d, k, tok, E, P, seq, steps, R=2, grad=True):
     """Back-to-back compress+decompress (and grad compress+decompress) over R
-    rotating buffer sets of device-drawn inputs; mean ms per pair."""
+    rotating buffer sets of device-drawn inputs; ms per pair (median of the
+    means of three timed runs)."""
     N = tok.shape[0]
     gen = torch.Generator(device="cuda")
     gen.manual_seed(N * 7 + d)
@@ -356,17 +357,23 @@ def _pair_times(sn, torch, basis, d, k, tok, E, P, seq, steps, R=2, grad=True):
     Os = [torch.empty(N, d, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     stream = torch.cuda.current_stream()
 
-    def loop(fn):
+    def loop(fn, blocks=3):
+        # median over `blocks` timed runs of `steps` pairs: one host-side
+        # stall inside a run (the GPU idles between launches) skews that
+        # run's mean, not the figure
         for i in range(3):
             fn(i % R)
         torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for i in range(steps):
-            fn(i % R)
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / steps
+        means = []
+        for _ in range(blocks):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(steps):
+                fn(i % R)
+            b.record(stream)
+            torch.cuda.synchronize()
+            means.append(a.elapsed_time(b) / steps)
+        return float(np.median(means))
 
     def fwd(j):
         sn.sn_compress(basis, Xs[j], tok=tok, E=E, P=P, seq_len=seq, out=Cs[j])
@@ -843,18 +850,22 @@ def main():
     # the write-backs the previous one left in the caches, which the per-op
     # event times inside the step can shift from one op to the next.
     def pair_loop(cname):
-        a, b = mk()
+        # median of three timed runs of K pairs (a host stall skews one run)
         for i in range(3):
             op(cname, i)
             op("decompress", i)
         torch.cuda.synchronize()
-        a.record(stream)
-        for i in range(K):
-            op(cname, args.warmup + i)
-            op("decompress", args.warmup + i)
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / K
+        means = []
+        for _ in range(3):
+            a, b = mk()
+            a.record(stream)
+            for i in range(K):
+                op(cname, args.warmup + i)
+                op("decompress", args.warmup + i)
+            b.record(stream)
+            torch.cuda.synchronize()
+            means.append(a.elapsed_time(b) / K)
+        return float(np.median(means))
 
     pair_ms = pair_loop("compress")
     ppair_ms = pair_loop("compress_projected")
