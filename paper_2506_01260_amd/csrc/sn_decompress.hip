@@ -123,14 +123,9 @@ __device__ __forceinline__ void add8(float (&o)[8], u32x4 v) {
   }
 }
 
-// LDS of a workgroup besides the U slice: the per-wave transpose buffers and,
-// when there are tables, the staged ids (a union-free pair of layouts so the
-// kernels without tables stay within two workgroups per CU at ks = 3).
-struct DSmemIds {
-  f32x4 ot[kDW][16 * 32];
-  int2 idl[kDW][kMaxWaveTiles][16];  // (token id, position id) per tile row
-};
-struct DSmemPlain {
+// LDS of a workgroup besides the U slice: the per-wave transpose buffers
+// (32 KiB; with the 48 KiB slice at ks = 3, two workgroups fill a CU's 160 KiB).
+struct DSmem {
   f32x4 ot[kDW][16 * 32];
 };
 
@@ -142,7 +137,7 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   constexpr int FR = 2 * KS;  // fragments per row group
   __shared__ u32x4 us[kPG * FR * 64];
   constexpr bool kIds = HE || HP;
-  __shared__ typename std::conditional<kIds, DSmemIds, DSmemPlain>::type sm;
+  __shared__ DSmem sm;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -169,35 +164,39 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     return t < tm.N ? t : tm.N - 1;
   };
 
-  // Stage the ids of all the wave's tiles in LDS up front (fixed trip count,
-  // clamped tiles: all loads are in flight before the first wait), each id
-  // already clamped into its table (out-of-range ids set a flag bit).
+  // Load the ids of all the wave's tiles up front (fixed trip count, clamped
+  // tiles: all loads are in flight before the first wait) and clamp each into
+  // its table (out-of-range ids set a flag bit).  They stay in registers:
+  // lane (g, n) holds row n of tiles 4 i + g in entry i, and the lanes that need
+  // a row fetch it with a cross-lane permute (no LDS allocation, so the
+  // tables cost no occupancy).
   int bad = 0;
+  static_assert(kMaxWaveTiles == 16, "four entries per lane");
+  // token ids e0..e3 and position ids q0..q3: plain scalars, never indexed
+  int e0 = 0, e1 = 0, e2 = 0, e3 = 0, q0 = 0, q1 = 0, q2 = 0, q3 = 0;
   if constexpr (kIds) {
     if (nt > 0) {
-    int2 v[kMaxWaveTiles / 4];
-#pragma unroll
-    for (int i = 0; i < kMaxWaveTiles / 4; ++i) {
-      const unsigned T = tile_of(4 * i + g);
-      const int t = token(T, n);
-      v[i] = int2{0, 0};
-      if (HE) v[i].x = ids.tok[t];
-      if (HP) {
-        if (ids.pos)
-          v[i].y = ids.pos[t];
-        else if (tm.batch > 0)
-          v[i].y = dtile_pos0(tm, T) + n;
-        else
-          v[i].y = static_cast<int>(static_cast<unsigned>(t) % static_cast<unsigned>(ids.seq_len));
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxWaveTiles / 4; ++i) {
-      if (HE) v[i].x = static_cast<int>(clamp_flag(v[i].x, ids.vocab, 1, bad));
-      if (HP) v[i].y = static_cast<int>(clamp_flag(v[i].y, ids.n_pos, 2, bad));
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxWaveTiles / 4; ++i) sm.idl[wave][4 * i + g][n] = v[i];
+      auto tok_id = [&](int i) {
+        return HE ? ids.tok[token(tile_of(4 * i + g), n)] : 0;
+      };
+      auto pos_id = [&](int i) {
+        if (!HP) return 0;
+        const unsigned T = tile_of(4 * i + g);
+        const int t = token(T, n);
+        if (ids.pos) return ids.pos[t];
+        if (tm.batch > 0) return dtile_pos0(tm, T) + n;
+        return static_cast<int>(static_cast<unsigned>(t) % static_cast<unsigned>(ids.seq_len));
+      };
+      e0 = tok_id(0); e1 = tok_id(1); e2 = tok_id(2); e3 = tok_id(3);
+      q0 = pos_id(0); q1 = pos_id(1); q2 = pos_id(2); q3 = pos_id(3);
+      auto ce = [&](int id) {
+        return HE ? static_cast<int>(clamp_flag(id, ids.vocab, 1, bad)) : 0;
+      };
+      auto cp = [&](int id) {
+        return HP ? static_cast<int>(clamp_flag(id, ids.n_pos, 2, bad)) : 0;
+      };
+      e0 = ce(e0); e1 = ce(e1); e2 = ce(e2); e3 = ce(e3);
+      q0 = cp(q0); q1 = cp(q1); q2 = cp(q2); q3 = cp(q3);
     }
   }
   {  // the block's U slice -> LDS, 1 KiB per direct-to-LDS load
@@ -220,17 +219,26 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
 
   auto load_tile = [&](DTile<KS> &dt, int j) {
     const unsigned T = tile_of(j);
-    const int jc = j < nt ? j : nt - 1;
     const int t0 = dtile_token0(tm, T);  // the tile's first token, once per tile
     auto tok_of = [&](int r) { return t0 + r < tm.N ? t0 + r : tm.N - 1; };
     load_coeffs<KS, CM>(dt, tok_of(n), C, ldc, k, g);
+    // Tiles are loaded in order 0, 1, 2, ...: every fourth tile the entries
+    // move down one, so tile j's ids are always in entry 0 (a wave-uniform
+    // branch and register moves; a choice among the entries by j / 4 would be
+    // compiled to an indexed access to private memory).  Past the last tile
+    // (j >= nt) entry 0 holds ids of the last staged tiles: valid rows, and
+    // the repeated tile is never stored.
+    if (j > 0 && (j & 3) == 0) {
+      e0 = e1; e1 = e2; e2 = e3;
+      q0 = q1; q1 = q2; q2 = q3;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = 4 * i + q;
-      if constexpr (kIds) {
-        const int2 v = sm.idl[wave][jc][r];  // clamped when staged
-        if (HE) dt.er[i] = v.x;
-        if (HP) dt.pr[i] = v.y;
+      if constexpr (kIds) {  // row r of tile j: lane 16 (j % 4) + r, entry 0
+        const int src = (16 * (j & 3) + r) * 4;
+        if (HE) dt.er[i] = __builtin_amdgcn_ds_bpermute(src, e0);
+        if (HP) dt.pr[i] = __builtin_amdgcn_ds_bpermute(src, q0);
       }
       dt.xr[i] = tok_of(r);
     }
