@@ -49,9 +49,9 @@ CALIB_BYTES = 256 * 1024 * 1024   # plain copy used to scale the HBM counters
 # rocprofv3 kernel names of each op (substring match on the demangled name)
 OP_KERNELS = {
     "compress": ["compress_kernel<3, true, true, 8, 8, 0>"],
-    "decompress": ["decompress_cb_kernel<2, true, true, 0>"],
+    "decompress": ["decompress_cb_kernel<2, true, true, 0, false>"],
     "grad_compress": ["compress_kernel<3, false, false, 1, 8, 0>"],
-    "grad_decompress": ["decompress_cb_kernel<2, false, false, 0>"],
+    "grad_decompress": ["decompress_cb_kernel<2, false, false, 0, false>"],
     "compress_projected": ["compress_kernel<3, false, false, 1, 8, 1>"],
     # subspace update: its compress pass and its contraction over tokens
     "grassmann_compress": ["compress_kernel<3, false, false, 1, 8, 3>"],

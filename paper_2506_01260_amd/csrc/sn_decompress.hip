@@ -129,7 +129,8 @@ struct DSmem {
   f32x4 ot[kDW][16 * 32];
 };
 
-template <int KS, bool HE, bool HP, int CM>
+// PS: load the P rows with non-temporal loads (each is read once per call).
+template <int KS, bool HE, bool HP, int CM, bool PS>
 __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     const bf16_t *__restrict__ rfrag, int64_t k, const bf16_t *__restrict__ C, int64_t ldc,
     DTiling tm, IdArgs ids, ColSegs xs, int ncb, int ntiles,
@@ -266,8 +267,13 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   };
   auto load_p = [&](PRows &pr, const DTile<KS> &dt, int c) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      pr.v[i] = ld16(row_at(Pb, dt.pr[i], ldp_b) + 128 * c);
+    for (int i = 0; i < 4; ++i) {
+      const bf16_t *src = row_at(Pb, dt.pr[i], ldp_b) + 128 * c;
+      if constexpr (PS)
+        pr.v[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src));
+      else
+        pr.v[i] = ld16(src);
+    }
   };
   // whether tile j has other positions than tile j - 1 (always, unless position-major)
   auto new_pos = [&](int j) {
@@ -357,20 +363,20 @@ int64_t resident_slots(K kernel) {
   return static_cast<int64_t>(cus) * per_cu;
 }
 
-template <int KS, bool HE, bool HP, int CM>
+template <int KS, bool HE, bool HP, int CM, bool PS = false>
 void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
                 const DTiling &tm, const IdArgs &ids, const ColSegs &X, hipStream_t s) {
   const int ncb = static_cast<int>(L.d / kDCols);
   const int64_t ntiles = ceil_div(tm.N, 16);
   // one round of resident workgroups over the whole grid, whole waves of tiles
-  static const int64_t slots = resident_slots(decompress_cb_kernel<KS, HE, HP, CM>);
+  static const int64_t slots = resident_slots(decompress_cb_kernel<KS, HE, HP, CM, PS>);
   const int64_t groups = slots / ncb > 0 ? slots / ncb : 1;  // token groups per round
   int64_t per = ceil_div(ntiles, groups);
   per = per < kDW ? kDW : (per > kDW * kMaxWaveTiles ? kDW * kMaxWaveTiles : per);
   per = ceil_div(per, kDW) * kDW;
   const int64_t tgroups = ceil_div(ntiles, per);
   dim3 grid(static_cast<unsigned>(tgroups * ncb));
-  decompress_cb_kernel<KS, HE, HP, CM><<<grid, kDThreads, 0, s>>>(
+  decompress_cb_kernel<KS, HE, HP, CM, PS><<<grid, kDThreads, 0, s>>>(
       rf, L.k, static_cast<const bf16_t *>(C), ldc, tm, ids, X, ncb,
       static_cast<int>(ntiles), static_cast<int>(per));
 }
@@ -379,7 +385,14 @@ template <int KS, int CM>
 void launch_dcb_t(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
                   const DTiling &tm, const IdArgs &ids, const ColSegs &X, hipStream_t s) {
   const bool he = ids.E != nullptr, hp = ids.P != nullptr;
-  if (he && hp)
+  // Each P row piece is read once per call.  Beside T_fixed, a large P
+  // (over 64 MiB) streams through the caches and evicts the T_fixed rows that
+  // are reused: it is loaded non-temporally (d = 8192: ~235 -> ~200 us at
+  // 32768 tokens).  Alone, or when small, it is loaded normally and stays in
+  // the 256 MB Infinity Cache from one call to the next.
+  if (he && hp && ids.n_pos * L.d * 2 > (int64_t{64} << 20))
+    launch_dcb<KS, true, true, CM, true>(rf, L, C, ldc, tm, ids, X, s);
+  else if (he && hp)
     launch_dcb<KS, true, true, CM>(rf, L, C, ldc, tm, ids, X, s);
   else if (he)
     launch_dcb<KS, true, false, CM>(rf, L, C, ldc, tm, ids, X, s);
