@@ -71,6 +71,7 @@ struct Tiling {
   int64_t N;
   int64_t seq;      // positions per sequence (position-major tiles only)
   int bp;           // batches per tile: 1 = token-major, else 4 or 8
+  int p_stream;     // copy the P rows non-temporally (beside T_fixed, a large P)
 };
 
 // Token of lane n of 16-token tile T (T already clamped to a valid tile);
@@ -159,6 +160,18 @@ __device__ __forceinline__ void dma_rows(const RowSet<R> &rs, int64_t col, u32x4
         static_cast<const void *>(rs.ptr[i] + col + 8 * (m ^ (r & 7))),
         (__attribute__((address_space(3))) void *)(dst + i * 64), 16, 0, STREAM ? 2 : 0);
   }
+}
+
+// dma_rows with the cache policy chosen at run time (a wave-uniform branch
+// between two copies whose policy operands differ, which the compiler
+// cannot fold into one).
+template <int R>
+__device__ __forceinline__ void dma_rows_rt(const RowSet<R> &rs, bool stream, int64_t col,
+                                            u32x4 *dst, int q, int m) {
+  if (stream)
+    dma_rows<R, true>(rs, col, dst, q, m);
+  else
+    dma_rows<R, false>(rs, col, dst, q, m);
 }
 
 // The first n (wave-uniform) copies of dma_rows.
@@ -357,11 +370,11 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
         dma_rows<kTokens, EPI != kEpiGrass>(rx, col, b + G::x_off, q, m);
       } else if (role == 1) {
         if (HE) dma_rows_n(re, ce, col, b + G::e_off, q, m);
-        if (HP && !G::p_with_u) dma_rows(rp, col, b + G::p_off, q, m);
+        if (HP && !G::p_with_u) dma_rows_rt(rp, tm.p_stream != 0, col, b + G::p_off, q, m);
       } else {
         dma_frags(kfrag + static_cast<int64_t>(st) * G::u_frags * 512, G::u_frags, b + G::u_off,
                   lane);
-        if (HP && G::p_with_u) dma_rows(rp, col, b + G::p_off, q, m);
+        if (HP && G::p_with_u) dma_rows_rt(rp, tm.p_stream != 0, col, b + G::p_off, q, m);
       }
     };
     for (int s = 0; s < NB - 1; ++s)
@@ -791,14 +804,19 @@ void launch_c_kt(const bf16_t *kf, const PackLayout &L, const void *X, int64_t l
   const int64_t N = tm.N;
   // position-major tiles (8 batches per tile, else 4) when whole workgroups
   // of tiles allow them
-  const Tiling tm8{N, ids.seq_len, 8}, tm4{N, ids.seq_len, 4};
+  const Tiling tm8{N, ids.seq_len, 8, 0}, tm4{N, ids.seq_len, 4, 0};
   if (he && hp) {
+    // Each P row is read once per call; beside T_fixed a large P (over
+    // 64 MiB) would evict the T_fixed rows that repeated ids reuse, so its
+    // rows are copied non-temporally.  A small P is kept in the caches.
+    const int ps = ids.n_pos * L.d * 2 > (int64_t{64} << 20) ? 1 : 0;
+    const Tiling s8{N, ids.seq_len, 8, ps}, s4{N, ids.seq_len, 4, ps}, s1{N, 1, 1, ps};
     if (pm_tiling_ok(N, ids, 8, pick_nw<KT, true, true, 8>(N)))
-      launch_c<KT, true, true, 8>(kf, L, X, ldx, tm8, ids, C, ldc, cvec, s);
+      launch_c<KT, true, true, 8>(kf, L, X, ldx, s8, ids, C, ldc, cvec, s);
     else if (pm_tiling_ok(N, ids, 4, pick_nw<KT, true, true, 4>(N)))
-      launch_c<KT, true, true, 4>(kf, L, X, ldx, tm4, ids, C, ldc, cvec, s);
+      launch_c<KT, true, true, 4>(kf, L, X, ldx, s4, ids, C, ldc, cvec, s);
     else
-      launch_c<KT, true, true, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
+      launch_c<KT, true, true, 1>(kf, L, X, ldx, s1, ids, C, ldc, cvec, s);
   } else if (he) {
     launch_c<KT, true, false, 1>(kf, L, X, ldx, tm, ids, C, ldc, cvec, s);
   } else {
