@@ -313,6 +313,39 @@ def test_tables_optional_and_explicit_positions(dtype):
                       dtype, f"decompress {name}")
 
 
+def test_large_positional_table_streamed():
+    """Both tables with a positional table over 64 MiB: compress and
+    decompress then load P's rows non-temporally (a kernel variant of the
+    decompress, a run-time copy policy of the compress).  Every element is
+    compared: default positions of two whole sequences (position-major
+    tiles) and explicit scattered positions over a ragged batch."""
+    d, k, seq = 4096, 40, 8208          # P: 8208 x 4096 bf16 = 67.2 MB > 64 MiB
+    n = 2 * seq
+    log(f"[streamed P] d={d} k={k} seq={seq} n={n}")
+    st, o, tok, _ = _small(d, k, n, vocab=300, seq=seq, seed=11)
+    basis = sn.sn_basis_pack(dev(st["U"]))
+    E, P, X, Cin = (dev(st[x]) for x in ("E", "P", "X", "C"))
+    t_tok = ids(tok)
+    C = sn.sn_compress(basis, X, tok=t_tok, E=E, P=P, seq_len=seq)
+    assert_parity(host(C), oracle.round_to(oracle.compress(o["X"], o["U"], tok, o["E"], o["P"],
+                                                           seq_len=seq), "bf16"),
+                  "bf16", "compress, default positions")
+    Xr = sn.sn_decompress(basis, Cin, tok=t_tok, E=E, P=P, seq_len=seq)
+    assert_parity(host(Xr), oracle.round_to(oracle.decompress(o["C"], o["U"], tok, o["E"], o["P"],
+                                                              seq_len=seq), "bf16"),
+                  "bf16", "decompress, default positions")
+    m = 1001                            # ragged, scattered explicit positions
+    pos = np.random.default_rng(12).integers(0, seq, m).astype(np.int32)
+    C = sn.sn_compress(basis, X[:m], tok=ids(tok[:m]), E=E, P=P, pos=ids(pos))
+    assert_parity(host(C), oracle.round_to(oracle.compress(o["X"][:m], o["U"], tok[:m], o["E"],
+                                                           o["P"], pos=pos), "bf16"),
+                  "bf16", "compress, explicit positions")
+    Xr = sn.sn_decompress(basis, Cin[:m], tok=ids(tok[:m]), E=E, P=P, pos=ids(pos))
+    assert_parity(host(Xr), oracle.round_to(oracle.decompress(o["C"][:m], o["U"], tok[:m],
+                                                              o["E"], o["P"], pos=pos), "bf16"),
+                  "bf16", "decompress, explicit positions")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_strides_and_guard_canaries(dtype):
     """Row strides larger than the row; nothing is written outside the N x k
