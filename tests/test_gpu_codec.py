@@ -323,8 +323,8 @@ def test_large_positional_table_streamed():
     n = 2 * seq
     log(f"[streamed P] d={d} k={k} seq={seq} n={n}")
     st, o, tok, _ = _small(d, k, n, vocab=300, seq=seq, seed=11)
-    basis = sn.sn_basis_pack(dev(st["U"]))
-    E, P, X, Cin = (dev(st[x]) for x in ("E", "P", "X", "C"))
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    E, P, X, Cin = (dev(st[x], "bf16") for x in ("E", "P", "X", "C"))
     t_tok = ids(tok)
     C = sn.sn_compress(basis, X, tok=t_tok, E=E, P=P, seq_len=seq)
     assert_parity(host(C), oracle.round_to(oracle.compress(o["X"], o["U"], tok, o["E"], o["P"],
