@@ -157,8 +157,10 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
   const int nt = T0 < T1 ? T1 - T0 : 0;  // this wave's tiles
 
   // Token of row r of the wave's j-th tile (clamped to the wave's last tile).
-  // Rows past the last token repeat token N-1: they load, compute and store
-  // exactly the bytes of row N-1, so every store is unconditional.
+  // Rows past the last token read the rows of token N-1 (every load stays in
+  // bounds).  Without P they compute and store exactly the bytes of row N-1
+  // again (unconditional stores); with P they are not stored, since in
+  // position-major order they may reuse another sequence's positional rows.
   auto tile_of = [&](int j) { return static_cast<unsigned>(T0 + (j < nt ? j : nt - 1)); };
   auto token = [&](unsigned T, int r) {
     const int t = dtile_token0(tm, T) + r;
@@ -185,7 +187,8 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
         const unsigned T = tile_of(4 * i + g);
         const int t = token(T, n);
         if (ids.pos) return ids.pos[t];
-        if (tm.batch > 0) return dtile_pos0(tm, T) + n;
+        if (tm.batch > 0 && dtile_token0(tm, T) + n < tm.N) return dtile_pos0(tm, T) + n;
+        // token-major order, or a row past N (its clamped token's position)
         return static_cast<int>(static_cast<unsigned>(t) % static_cast<unsigned>(ids.seq_len));
       };
       e0 = tok_id(0); e1 = tok_id(1); e2 = tok_id(2); e3 = tok_id(3);
@@ -241,7 +244,10 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
         if (HE) dt.er[i] = __builtin_amdgcn_ds_bpermute(src, e0);
         if (HP) dt.pr[i] = __builtin_amdgcn_ds_bpermute(src, q0);
       }
-      dt.xr[i] = tok_of(r);
+      if constexpr (HP)
+        dt.xr[i] = t0 + r < tm.N ? t0 + r : -1;  // -1: past N, not stored
+      else
+        dt.xr[i] = tok_of(r);
     }
   };
   const char *Eb = reinterpret_cast<const char *>(static_cast<const bf16_t *>(ids.E) + col_r);
@@ -311,10 +317,12 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
       // Non-temporal store: X is written once and not read back here, and
       // keeping it out of the caches leaves L2 to the gathered rows (the
       // gathers' hit rate, and with it the kernel time, depends on it).
-      __builtin_nontemporal_store(
-          u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
-                pack_bf16x2(o[6], o[7])},
-          reinterpret_cast<u32x4 *>(const_cast<bf16_t *>(row_at(Xb, dt.xr[i], ldx_b)) + 128 * c));
+      if (!HP || dt.xr[i] >= 0)
+        __builtin_nontemporal_store(
+            u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                  pack_bf16x2(o[6], o[7])},
+            reinterpret_cast<u32x4 *>(const_cast<bf16_t *>(row_at(Xb, dt.xr[i], ldx_b)) +
+                                      128 * c));
     }
   };
 
@@ -367,7 +375,10 @@ template <int KS, bool HE, bool HP, int CM, bool PS = false>
 void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ldc,
                 const DTiling &tm, const IdArgs &ids, const ColSegs &X, hipStream_t s) {
   const int ncb = static_cast<int>(L.d / kDCols);
-  const int64_t ntiles = ceil_div(tm.N, 16);
+  // position-major tiles cover whole [batch, seq] sequences (the last one may
+  // be short: its missing rows are read but not stored)
+  const int64_t ntiles = tm.batch > 0 ? static_cast<int64_t>(tm.batch) * (tm.seq / 16)
+                                      : ceil_div(tm.N, 16);
   // one round of resident workgroups over the whole grid, whole waves of tiles
   static const int64_t slots = resident_slots(decompress_cb_kernel<KS, HE, HP, CM, PS>);
   const int64_t groups = slots / ncb > 0 ? slots / ncb : 1;  // token groups per round
@@ -447,10 +458,14 @@ hipError_t launch_decompress_mfma_segs(const PackLayout &L, const void *packed, 
                     : (ca & 3) == 0 && ldc % 2 == 0 && L.k % 2 == 0 ? 1
                                                                     : 2;
   DTiling tm{static_cast<int>(N), 0, 0};
-  // position-major order for the default positions of whole [batch, seq] rows
-  if (ids.P && !ids.pos && ids.seq_len % 16 == 0 && N % ids.seq_len == 0) {
+  // position-major order for the default positions of [batch, seq] rows; a
+  // short last sequence is allowed while the rows it lacks (read, not
+  // stored) are at most an eighth of a sequence
+  if (ids.P && !ids.pos && ids.seq_len % 16 == 0 && N >= ids.seq_len &&
+      (ceil_div(N, ids.seq_len) * ids.seq_len - N) * 8 <= ids.seq_len &&
+      ceil_div(N, ids.seq_len) * ids.seq_len <= INT32_MAX) {
     tm.seq = static_cast<int>(ids.seq_len);
-    tm.batch = static_cast<int>(N / ids.seq_len);
+    tm.batch = static_cast<int>(ceil_div(N, ids.seq_len));
   }
   switch (L.ks) {
     case 1: launch_dcb_ks<1>(rf, L, C, ldc, cmode, tm, ids, X, s); break;

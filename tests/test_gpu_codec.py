@@ -313,6 +313,30 @@ def test_tables_optional_and_explicit_positions(dtype):
                       dtype, f"decompress {name}")
 
 
+@pytest.mark.parametrize("n", [187, 184, 183, 511, 512])
+def test_decompress_short_last_sequence(n):
+    """Default positions of [batch, seq] rows whose last sequence is short
+    (seq = 64: 5, 8, 9, 1 and 0 rows missing).  Up to an eighth of a
+    sequence missing, the decompress keeps position-major tiles over whole
+    sequences and does not store the missing rows; beyond that it takes
+    token-major tiles.  Every element against the oracle, rows past N
+    untouched, no out-of-range flag."""
+    d, k, seq = 256, 20, 64
+    log(f"[short last sequence] n={n}")
+    st, o, tok, _ = _small(d, k, n, vocab=40, seq=seq, seed=n)
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    E, P, Cin = (dev(st[x], "bf16") for x in ("E", "P", "C"))
+    for name, gk, ok in [("E+P", dict(tok=ids(tok), E=E), dict(tok=tok, E=o["E"])),
+                         ("P only", {}, {})]:
+        big = torch.full((n + 64, d), 3.0, dtype=torch.bfloat16, device="cuda")
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        sn.sn_decompress(basis, Cin, P=P, seq_len=seq, out=big[:n], err_flag=flag, **gk)
+        ref = oracle.decompress(o["C"], o["U"], P=o["P"], seq_len=seq, **ok)
+        assert_parity(host(big[:n]), oracle.round_to(ref, "bf16"), "bf16", f"{name} n={n}")
+        assert bool((big[n:] == 3.0).all()), f"{name}: rows past N were written"
+        assert int(flag.item()) == 0, f"{name}: out-of-range flag {int(flag.item())}"
+
+
 def test_large_positional_table_streamed():
     """Both tables with a positional table over 64 MiB: compress and
     decompress then load P's rows non-temporally (a kernel variant of the
