@@ -80,14 +80,12 @@ def test_adamw_matches_oracle(dtype, rows, cols, t0, steps, subspace):
 
 
 @pytest.mark.parametrize("rows,cols", [(4096, 14336), (4096, 4096)])
-def test_adamw_full_size_sampled_columns(rows, cols):
-    """W2 and Wo of config 2: the step on the whole matrix, compared on sampled
-    columns (each column's step depends only on that column)."""
+def test_adamw_full_size(rows, cols):
+    """W2 and Wo of config 2: the modified step on the whole matrix, every
+    element of W, M and V compared."""
     log(f"[adamw full] {rows}x{cols}")
-    rng = np.random.default_rng(cols)
-    sel = np.unique(np.r_[0, cols - 1, rng.integers(0, cols, 62)])
-    got, ref = _case("bf16", rows, cols, 3, 1, True, cols_sel=sel, cfg_id=2)
-    _check(got, ref, "bf16", f"bf16 {rows}x{cols} sampled")
+    got, ref = _case("bf16", rows, cols, 3, 1, True, cfg_id=2)
+    _check(got, ref, "bf16", f"bf16 {rows}x{cols}")
 
 
 def test_subspace_step_keeps_columns_in_s():
