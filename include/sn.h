@@ -20,8 +20,10 @@
  * ----------------------------------------
  * - Every matrix is row-major; "ld" arguments are row strides in ELEMENTS.
  * - All array pointers are DEVICE pointers (HIP device memory of the current
- *   device) unless stated otherwise.  The library never allocates, frees or
- *   keeps a pointer after a call returns; the caller owns every buffer.
+ *   device) unless stated otherwise.  No call allocates or frees memory, and
+ *   none keeps a caller's pointer after it returns; the caller owns every
+ *   buffer (the one memory of the library's own is the static scratch of
+ *   sn_project_weights_noalloc, part of its loaded code).
  * - dt (sn_dtype) is the element type of every float array of the call
  *   (U, X, G, E, P, C, W): all SN_F32 or all SN_BF16.  Accumulation is fp32;
  *   each output element is rounded once (round to nearest even) to dt.
@@ -212,6 +214,27 @@ size_t sn_project_weights_workspace_bytes(int64_t d, int64_t k, int32_t dt, int6
 int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt,
                            void *W, int64_t m, int64_t ldw,
                            void *workspace, size_t workspace_bytes, sn_stream stream);
+
+/* sn_project_weights_noalloc: sn_project_weights with no workspace argument,
+ * for callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid allocation).
+ *
+ *   basis, d, k, dt, W, m, ldw, stream: as in sn_project_weights (same
+ *   kernels, same result bit for bit).
+ * The workspace is a static device array of SN_PROJECT_NOALLOC_SCRATCH_BYTES
+ * inside the library: every device the library runs on holds one copy for
+ * the life of the process.  A call whose sn_project_weights_workspace_bytes
+ * exceeds it returns SN_ERR_WORKSPACE before anything is launched (at
+ * d = 4096, k = 40 that allows m up to ~49,000 columns; at d = 8192, k = 82,
+ * m up to ~12,000).  The call allocates and frees nothing; the first call on
+ * a device looks up that device's copy of the array.  All calls on one device
+ * share its array: calls that overlap in time on the same device (other
+ * streams, other host threads) race and must be ordered by the caller.
+ * Errors: as sn_project_weights, plus WORKSPACE for a matrix too large for
+ * the scratch and HIP when the scratch cannot be located. */
+#define SN_PROJECT_NOALLOC_SCRATCH_BYTES (128u << 20)
+int32_t sn_project_weights_noalloc(const void *basis, int64_t d, int64_t k, int32_t dt,
+                                   void *W, int64_t m, int64_t ldw, sn_stream stream);
 
 /* Several weights confined in one call (the optimizer step's sweep over a
  * layer's or a model's projection matrices, Sec. 5): W[i] (d x m[i], row

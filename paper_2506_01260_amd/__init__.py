@@ -60,6 +60,7 @@ _SIGNATURES = {
                                      _I64, _I64, _P, _I64, _P, _P]),
     "sn_project_weights_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I64]),
     "sn_project_weights": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P, _SZ, _P]),
+    "sn_project_weights_noalloc": (_I32, [_P, _I64, _I64, _I32, _P, _I64, _I64, _P]),
     "sn_project_weights_multi_workspace_bytes": (_SZ, [_I64, _I64, _I32, _I32, _P]),
     "sn_project_weights_multi": (_I32, [_P, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _SZ, _P]),
     "sn_grassmann_state_bytes": (_SZ, [_I64, _I64]),
@@ -340,6 +341,18 @@ def sn_project_weights(basis: Basis, W: torch.Tensor, workspace=None, stream=Non
         raise SnError(9, f"workspace needs {need} device bytes")
     _check(lib().sn_project_weights(basis.ptr, d, basis.k, basis.dt, wp, m, ldw,
                                     workspace.data_ptr(), workspace.numel(), _stream(stream)))
+    return W
+
+
+def sn_project_weights_noalloc(basis: Basis, W: torch.Tensor, stream=None) -> torch.Tensor:
+    """W <- U (U^T W) in place with the library's static scratch (no workspace,
+    no allocation); returns W."""
+    wp, d, m, ldw = _mat(W, "W")
+    if d != basis.d:
+        raise SnError(2, f"W has {d} rows, basis has d = {basis.d}")
+    _same_dtype(basis, ("W", W))
+    _check(lib().sn_project_weights_noalloc(basis.ptr, d, basis.k, basis.dt, wp, m, ldw,
+                                            _stream(stream)))
     return W
 
 

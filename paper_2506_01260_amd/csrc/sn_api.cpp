@@ -28,6 +28,23 @@ int32_t ok() {
   return SN_OK;
 }
 
+}  // namespace
+
+
+namespace sn {
+
+int32_t set_error(int32_t st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+}  // namespace sn
+
+namespace {
+
 int32_t hip_status(hipError_t e, const char *what) {
   if (e == hipSuccess) return ok();
   return fail(SN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -161,6 +178,22 @@ sn::IdArgs make_ids(const int32_t *tok, const void *E, int64_t vocab, int64_t ld
 }
 
 }  // namespace
+
+namespace sn {
+
+int32_t project_args_check(const void *basis, int64_t d, int64_t k, int32_t dt, const void *W,
+                           int64_t m, int64_t ldw) {
+  int32_t st = check_basis(basis, d, k, dt);
+  if (st) return st;
+  if (m < 0 || m >= kMaxDim) return fail(SN_ERR_SHAPE, "m out of range");
+  if (ldw < m || ldw >= kMaxDim) return fail(SN_ERR_SHAPE, "ldw must be >= m");
+  if (m == 0) return ok();
+  if (!W) return fail(SN_ERR_NULL, "W is NULL");
+  if (!elem_aligned(W, dt)) return fail(SN_ERR_ALIGN, "W not aligned to its element size");
+  return ok();
+}
+
+}  // namespace sn
 
 extern "C" {
 
@@ -384,13 +417,10 @@ size_t sn_project_weights_workspace_bytes(int64_t d, int64_t k, int32_t dt, int6
 int32_t sn_project_weights(const void *basis, int64_t d, int64_t k, int32_t dt, void *W,
                            int64_t m, int64_t ldw, void *workspace, size_t workspace_bytes,
                            sn_stream stream) {
-  int32_t st = check_basis(basis, d, k, dt);
+  int32_t st = sn::project_args_check(basis, d, k, dt, W, m, ldw);
   if (st) return st;
-  if (m < 0 || m >= kMaxDim) return fail(SN_ERR_SHAPE, "m out of range");
-  if (ldw < m || ldw >= kMaxDim) return fail(SN_ERR_SHAPE, "ldw must be >= m");
   if (m == 0) return ok();
-  if (!W || !workspace) return fail(SN_ERR_NULL, "W or workspace is NULL");
-  if (!elem_aligned(W, dt)) return fail(SN_ERR_ALIGN, "W not aligned to its element size");
+  if (!workspace) return fail(SN_ERR_NULL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 255)
     return fail(SN_ERR_ALIGN, "workspace must be 256-byte aligned");
   const size_t need = sn_project_weights_workspace_bytes(d, k, dt, m);

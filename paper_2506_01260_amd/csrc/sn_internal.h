@@ -203,4 +203,11 @@ hipError_t launch_project_mfma_segs(const PackLayout &L, const void *packed, con
 hipError_t launch_project_mfma(const PackLayout &L, const void *packed, void *W, int64_t m,
                                int64_t ldw, void *ws, hipStream_t s);
 
+// Record a message for sn_last_error() on the calling thread; returns st.
+int32_t set_error(int32_t st, const char *fmt, ...);
+// sn_project_weights' checks of everything but the workspace (SN_OK or the
+// status, with the message recorded).
+int32_t project_args_check(const void *basis, int64_t d, int64_t k, int32_t dt, const void *W,
+                           int64_t m, int64_t ldw);
+
 }  // namespace sn

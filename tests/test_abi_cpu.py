@@ -290,3 +290,20 @@ def test_project_multi_validation():
     assert call(Wp=overlapping) == 5
     assert call(w=FAKE + (2 << 24)) == 5              # workspace overlaps W[1]
     assert call(count=0) == 0
+
+
+def test_project_noalloc_validation():
+    """The no-alloc projection checks every argument before touching a device,
+    including a matrix too large for its static scratch."""
+    f = sn.lib().sn_project_weights_noalloc
+    W = FAKE + (1 << 20)
+    assert f(None, 256, 8, 1, W, 64, 64, None) == 1            # basis NULL
+    assert f(FAKE, 256, 8, 1, None, 64, 64, None) == 1         # W NULL
+    assert f(FAKE, 256, 8, 1, W, 64, 63, None) == 2            # ldw < m
+    assert f(FAKE, 256, 8, 7, W, 64, 64, None) == 3            # dtype
+    assert f(FAKE, 256, 8, 1, W + 1, 64, 64, None) == 4        # misaligned bf16 pointer
+    assert f(FAKE, 256, 8, 1, None, 0, 0, None) == 0           # m == 0: no-op
+    m = 1 << 16
+    assert sn.lib().sn_project_weights_workspace_bytes(4096, 40, 1, m) > (128 << 20)
+    assert f(FAKE, 4096, 40, 1, W, m, m, None) == 9            # beyond the static scratch
+    assert b"static scratch" in sn.lib().sn_last_error()
