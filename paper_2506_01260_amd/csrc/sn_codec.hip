@@ -75,7 +75,9 @@ struct Tiling {
 };
 
 // Token of lane n of 16-token tile T (T already clamped to a valid tile);
-// token-major tiles past N repeat token N-1.
+// token-major tiles past N repeat token N-1.  Position-major tiles cover
+// whole sequences, so when the last sequence is short they name tokens at or
+// past N: those rows are loaded as token N-1 (load_token) and never stored.
 __device__ __forceinline__ int64_t tile_token(const Tiling &tm, int64_t T, int n) {
   if (tm.bp == 1) {
     const int64_t t = 16 * T + n;
@@ -85,6 +87,19 @@ __device__ __forceinline__ int64_t tile_token(const Tiling &tm, int64_t T, int n
   const int64_t tpb = tm.seq / pg;
   const int64_t bg = T / tpb, pt = T - bg * tpb;
   return (bg * tm.bp + n % tm.bp) * tm.seq + pt * pg + n / tm.bp;
+}
+
+// The token whose rows lane n of tile T loads (always below N).
+__device__ __forceinline__ int64_t load_token(const Tiling &tm, int64_t T, int n) {
+  const int64_t t = tile_token(tm, T, n);
+  return t < tm.N ? t : tm.N - 1;
+}
+
+// Tiles of a launch: token-major ceil(N / 16); position-major whole
+// sequences, ceil(N / seq) of them (bp x 16 / bp = 16 tokens per tile).
+__host__ __device__ __forceinline__ int64_t tile_count(const Tiling &tm) {
+  if (tm.bp == 1) return (tm.N + 15) / 16;
+  return (tm.N + tm.seq - 1) / tm.seq * (tm.seq / 16);
 }
 
 // First position of position-major tile T.
@@ -258,7 +273,7 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
   const int nst = static_cast<int>(d / kStageCols);
   const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nst));
   auto phys = [&](int si) { const int v = si + rot; return v >= nst ? v - nst : v; };
-  const int64_t ntiles = (tm.N + 15) / 16;
+  const int64_t ntiles = tile_count(tm);
   const int64_t T0 = static_cast<int64_t>(blockIdx.x) * NW;
 
   if (wave >= NW) {  // ------------------------------------------------ producers
@@ -269,11 +284,12 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
     const int q = lane / kPieces, m = lane % kPieces;
     RowSet<kTokens> rx, re;
     RowSet<G::dma_p * kRowsPerCopy> rp;
-    // token row r = 16 w + n of the workgroup (tiles past the end repeat the last)
+    // token row r = 16 w + n of the workgroup (tiles past the end repeat the
+    // last; rows past N load token N - 1)
     auto token_of = [&](int r) {
       int64_t T = T0 + r / 16;
       T = T < ntiles ? T : ntiles - 1;
-      return tile_token(tm, T, r % 16);
+      return load_token(tm, T, r % 16);
     };
     if (role == 0) {
 #pragma unroll
@@ -502,6 +518,7 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
   const int64_t i = 16 * T + n;
   const int64_t tok = tm.bp == 1 ? i : tile_token(tm, T, n);
   if (tm.bp == 1 && i >= tm.N) return;
+  if (tok >= tm.N) return;  // a row past N of a short last sequence
   if constexpr (EPI == kEpiGrass) {
 #pragma unroll
     for (int t = 0; t < KT; ++t)
@@ -710,12 +727,16 @@ bool tables_ok(const IdArgs &ids) {
 
 // Position-major tiling when the positions are the default i mod seq_len of a
 // row-major [batch, seq_len] batch with batch a multiple of 4 (8 preferred)
-// and whole workgroups of nw tiles.
+// and whole workgroups of nw tiles.  The last sequence may be short by at
+// most an eighth of a sequence: the tiles cover whole sequences and the
+// missing rows are loaded (as token N - 1) but not stored.
 bool pm_tiling_ok(int64_t N, const IdArgs &ids, int bp, int nw) {
-  if (!ids.P || ids.pos || ids.seq_len <= 0 || N % ids.seq_len != 0 || N % 16 != 0) return false;
-  const int64_t batch = N / ids.seq_len;
-  // every workgroup holds nw full tiles: N / 16 must be a multiple of nw
-  return batch % bp == 0 && ids.seq_len % (16 / bp) == 0 && (N / 16) % nw == 0;
+  if (!ids.P || ids.pos || ids.seq_len <= 0 || N <= 0) return false;
+  const int64_t seq = ids.seq_len;
+  const int64_t batch = ceil_div(N, seq);
+  if ((batch * seq - N) * 8 > seq) return false;
+  // every workgroup holds nw full tiles: batch x seq / 16 must be a multiple of nw
+  return batch % bp == 0 && seq % (16 / bp) == 0 && (batch * seq / 16) % nw == 0;
 }
 
 // Compute units of the current device (cached per device; concurrent first
@@ -750,7 +771,7 @@ template <int KT, bool HE, bool HP, int BP, int EPI = kEpiBf16>
 void launch_c(const bf16_t *kf, const PackLayout &L, const void *X, int64_t ldx, const Tiling &tm,
               const IdArgs &ids, void *C, int64_t ldc, int cvec, hipStream_t s,
               const ProjArgs &pa = ProjArgs{}, const GrassOut &go = GrassOut{}) {
-  const int64_t ntiles = (tm.N + 15) / 16;
+  const int64_t ntiles = tile_count(tm);
   if constexpr (nw_of<KT, HE, HP, BP>() == 8) {
     if (pick_nw<KT, HE, HP, BP>(tm.N) == 8) {
       compress_kernel<KT, HE, HP, BP, 8, EPI>

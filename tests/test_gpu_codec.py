@@ -400,6 +400,32 @@ def test_decompress_short_last_sequence(n):
         assert int(flag.item()) == 0, f"{name}: out-of-range flag {int(flag.item())}"
 
 
+@pytest.mark.parametrize("n,batch", [(256, 4), (255, 4), (249, 4), (248, 4), (247, 4),
+                                     (512, 8), (511, 8), (504, 8), (503, 8)])
+def test_compress_short_last_sequence(n, batch):
+    """Default positions of [batch, seq] rows (seq = 64) whose last sequence
+    is short by 0, 1, 7, 8 or 9 rows.  Up to an eighth of a sequence missing,
+    the compress keeps position-major tiles over whole sequences (the missing
+    rows are loaded as the last token's and not stored); beyond that it takes
+    token-major tiles.  Every element against the oracle, rows past N of the
+    output untouched, no out-of-range flag."""
+    d, k, seq = 256, 40, 64
+    assert batch * seq - 9 <= n <= batch * seq
+    log(f"[compress short last sequence] n={n} batch={batch}")
+    st, o, tok, _ = _small(d, k, n, vocab=40, seq=seq, seed=n + 1000)
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    E, P, X = (dev(st[x], "bf16") for x in ("E", "P", "X"))
+    for name, gk, ok in [("E+P", dict(tok=ids(tok), E=E), dict(tok=tok, E=o["E"])),
+                         ("P only", {}, {})]:
+        big = torch.full((n + 16, k), 3.0, dtype=torch.bfloat16, device="cuda")
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        sn.sn_compress(basis, X, P=P, seq_len=seq, out=big[:n], err_flag=flag, **gk)
+        ref = oracle.compress(o["X"], o["U"], P=o["P"], seq_len=seq, **ok)
+        assert_parity(host(big[:n]), oracle.round_to(ref, "bf16"), "bf16", f"{name} n={n}")
+        assert bool((big[n:] == 3.0).all()), f"{name}: rows past N were written"
+        assert int(flag.item()) == 0, f"{name}: out-of-range flag {int(flag.item())}"
+
+
 def test_large_positional_table_streamed():
     """Both tables with a positional table over 64 MiB: compress and
     decompress then load P's rows non-temporally (a kernel variant of the
