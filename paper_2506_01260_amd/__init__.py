@@ -30,7 +30,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsn.so")
+# SN_LIBRARY names another build of the same C ABI (the host-sanitizer build
+# of the CPU tests); by default the library built next to this file.
+LIB_PATH = os.environ.get("SN_LIBRARY") or os.path.join(_HERE, "libsn.so")
 
 SN_F32, SN_BF16 = 0, 1
 SN_ERR_INDEX = 6
@@ -83,6 +85,25 @@ _SIGNATURES = {
     "sn_last_error": (ctypes.c_char_p, []),
     "sn_version": (ctypes.c_char_p, []),
 }
+
+
+# Id checking (debug / test mode): the kernels clamp out-of-range token and
+# position ids and report them only through a device flag.  With checking on
+# (set_check_ids(True), or SN_CHECK_IDS=1 in the environment) every call that
+# takes ids gets a private flag, waits for the call to finish, ORs the flag
+# into the caller's err_flag (if any) and raises SnError(SN_ERR_INDEX) when an
+# id was out of range.  The wait serialises the stream: for tests and
+# debugging, not for production loops.
+_CHECK_IDS = os.environ.get("SN_CHECK_IDS", "") not in ("", "0")
+
+
+def set_check_ids(on: bool = True) -> None:
+    global _CHECK_IDS
+    _CHECK_IDS = bool(on)
+
+
+def check_ids_enabled() -> bool:
+    return _CHECK_IDS
 
 
 class SnError(RuntimeError):
@@ -142,6 +163,28 @@ def _ids(t, name, n):
             (n > 1 and t.stride(0) != 1):
         raise SnError(2, f"{name} must be a contiguous int32 device vector of length {n}")
     return t.data_ptr()
+
+
+def _id_flag(err_flag, device):
+    """(flag to pass to the C call, private flag or None): the caller's flag
+    itself, or with checking on a private zeroed flag."""
+    if not _CHECK_IDS:
+        return err_flag, None
+    own = torch.zeros(1, dtype=torch.int32, device=device)
+    return own, own
+
+
+def _id_check(own, caller, what: str):
+    """With checking on (own = the private flag): pass the bits on to the
+    caller's flag and raise if any id was out of range."""
+    if own is None:
+        return
+    if caller is not None:
+        caller.bitwise_or_(own)
+    bits = int(own.item())  # waits for the call
+    if bits:
+        raise SnError(SN_ERR_INDEX, f"{what}: out-of-range ids were clamped (flag bits {bits}: "
+                                    f"1 = token id, 2 = position id)")
 
 
 def _stream(stream):
@@ -219,9 +262,11 @@ def sn_compress(basis: Basis, X: torch.Tensor, tok=None, E=None, P=None, pos=Non
     _out_shape(out, (N, basis.k), "out")
     _same_dtype(basis, ("X", X), ("E", E), ("P", P), ("out", out))
     cp, _, _, ldc = _mat(out, "out")
+    flag, own = _id_flag(err_flag, X.device)
     _check(lib().sn_compress(basis.ptr, basis.d, basis.k, basis.dt, xp, N, ldx,
                              *_tables(N, tok, E, pos, P, seq_len), cp, ldc,
-                             None if err_flag is None else err_flag.data_ptr(), _stream(stream)))
+                             None if flag is None else flag.data_ptr(), _stream(stream)))
+    _id_check(own, err_flag, "sn_compress")
     return out
 
 
@@ -237,10 +282,12 @@ def sn_decompress(basis: Basis, C: torch.Tensor, tok=None, E=None, P=None, pos=N
     _out_shape(out, (N, basis.d), "out")
     _same_dtype(basis, ("C", C), ("E", E), ("P", P), ("out", out))
     xp, _, _, ldx = _mat(out, "out")
+    flag, own = _id_flag(err_flag, C.device)
     _check(lib().sn_decompress(basis.ptr, basis.d, basis.k, basis.dt, cp, N, ldc,
                                *_tables(N, tok, E, pos, P, seq_len), xp, ldx,
-                               None if err_flag is None else err_flag.data_ptr(),
+                               None if flag is None else flag.data_ptr(),
                                _stream(stream)))
+    _id_check(own, err_flag, "sn_decompress")
     return out
 
 
@@ -316,11 +363,13 @@ def sn_compress_projected(basis: Basis, X: torch.Tensor, proj: Projected, tok=No
     cp, _, _, ldc = _mat(out, "out")
     tok_ptr = _ids(tok, "tok", N) if proj.vocab else None
     pos_ptr = _ids(pos, "pos", N) if proj.n_pos else None
+    flag, own = _id_flag(err_flag, X.device)
     _check(lib().sn_compress_projected(basis.ptr, basis.d, basis.k, basis.dt, xp, N, ldx,
                                        tok_ptr, pos_ptr, int(seq_len or 0), proj.ptr,
                                        proj.vocab, proj.n_pos, cp, ldc,
-                                       None if err_flag is None else err_flag.data_ptr(),
+                                       None if flag is None else flag.data_ptr(),
                                        _stream(stream)))
+    _id_check(own, err_flag, "sn_compress_projected")
     return out
 
 
@@ -513,12 +562,14 @@ def sn_embed_lowrank_forward(basis: Basis, CS: torch.Tensor, tok: torch.Tensor, 
     need = sn_embed_lowrank_workspace_bytes(basis.d, basis.k, basis.dt, N, vocab)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=CS.device)
+    flag, own = _id_flag(err_flag, CS.device)
     _check(lib().sn_embed_lowrank_forward(basis.ptr, basis.d, basis.k, basis.dt, cp, vocab, ldcs,
                                           tok_ptr, e_ptr, lde, pos_ptr, p_ptr, n_pos, ldp, sl,
                                           xp, N, ldx,
-                                          None if err_flag is None else err_flag.data_ptr(),
+                                          None if flag is None else flag.data_ptr(),
                                           workspace.data_ptr(), workspace.numel(),
                                           _stream(stream)))
+    _id_check(own, err_flag, "sn_embed_lowrank_forward")
     return out
 
 
@@ -535,11 +586,13 @@ def sn_embed_lowrank_backward(basis: Basis, dX0: torch.Tensor, tok: torch.Tensor
     need = sn_embed_lowrank_workspace_bytes(basis.d, basis.k, basis.dt, N, vocab)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dX0.device)
+    flag, own = _id_flag(err_flag, dX0.device)
     _check(lib().sn_embed_lowrank_backward(basis.ptr, basis.d, basis.k, basis.dt, gp, N, ldg,
                                            tok_ptr, vocab, cp, ldgc,
-                                           None if err_flag is None else err_flag.data_ptr(),
+                                           None if flag is None else flag.data_ptr(),
                                            workspace.data_ptr(), workspace.numel(),
                                            _stream(stream)))
+    _id_check(own, err_flag, "sn_embed_lowrank_backward")
     return gCS
 
 

@@ -66,5 +66,47 @@ def build(jobs: int = 8) -> str:
     return LIB
 
 
+# ---------------------------------------------------------------------------
+# Host sanitizers: the C ABI's validation code (sn_api.cpp) built with g++
+# under AddressSanitizer and UndefinedBehaviorSanitizer, linked with the
+# regular (uninstrumented) kernel objects.  Only host code is instrumented;
+# the library it makes is for the CPU tests of the argument checks
+# (LD_PRELOAD the ASan runtime and point SN_LIBRARY at it).
+SAN_LIB = os.path.join(BUILD, "libsn_hostsan.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+             "-fno-omit-frame-pointer", "-g", "-O1"]
+
+
+def build_host_sanitized() -> str:
+    """Build _build/libsn_hostsan.so: sn_api.cpp under ASan + UBSan (g++),
+    the kernel objects from the regular build (compiled first if missing or
+    older than their sources)."""
+    gxx = shutil.which("g++")
+    if not gxx:
+        raise RuntimeError("g++ not found")
+    hips = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    objs = [os.path.join(BUILD, os.path.basename(h) + ".o") for h in hips]
+    headers = glob.glob(os.path.join(CSRC, "*.h")) + [os.path.join(INCLUDE, "sn.h")]
+    newest_h = max(os.path.getmtime(h) for h in headers)
+    stale = [o for h, o in zip(hips, objs)
+             if not os.path.exists(o) or os.path.getmtime(o) < max(os.path.getmtime(h), newest_h)]
+    if stale:
+        build()
+    os.makedirs(BUILD, exist_ok=True)
+    api_obj = os.path.join(BUILD, "sn_api.hostsan.o")
+    cmd = [gxx, "-std=c++17", "-fPIC", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+           f"-I{INCLUDE}", f"-I{CSRC}", *SAN_FLAGS, "-c", os.path.join(CSRC, "sn_api.cpp"),
+           "-o", api_obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stderr}")
+    cmd = [gxx, "-shared", "-fPIC", *SAN_FLAGS, api_obj, *objs, "-L/opt/rocm/lib",
+           "-Wl,-rpath,/opt/rocm/lib", "-lamdhip64", "-o", SAN_LIB]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stderr}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     print(build())

@@ -275,8 +275,16 @@ __global__ __launch_bounds__(256) void project_pass2_rfrag_kernel(
   bf16_t v0 = bf16_t(0), v1 = bf16_t(0);
   int j0, j1;
   if (j < k) {
+    // every split's value first (independent loads in flight together), then
+    // the fixed-order compensated sum; dsplit <= 8
+    float t[8];
+#pragma unroll
+    for (int sp = 0; sp < 8; ++sp)
+      t[sp] = sp < dsplit ? Tp[((sp < dsplit ? sp : 0) * m_pad + c) * kp + j] : 0.0f;
     Dot2 acc;
-    for (int sp = 0; sp < dsplit; ++sp) acc.add(Tp[(sp * m_pad + c) * kp + j]);
+#pragma unroll
+    for (int sp = 0; sp < 8; ++sp)
+      if (sp < dsplit) acc.add(t[sp]);
     const float v = acc.value();
     v0 = from_f32<bf16_t>(v);
     v1 = from_f32<bf16_t>(v - to_f32(v0));

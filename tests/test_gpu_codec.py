@@ -687,3 +687,36 @@ def test_project_weights_multi(dtype, d, k, widths, pad):
                            f"W[{i}] ({d}x{m}) every column")
         if pad:  # the padding columns are untouched
             assert float(Ws[i].as_strided((d, pad), (m + pad, 1), m).abs().max()) == 0.0
+
+
+def test_id_check_mode_raises_index_error():
+    """With id checking on, a call with an out-of-range id raises
+    SnError(SN_ERR_INDEX) after the call, the caller's flag still receives
+    the bits, and in-range ids raise nothing."""
+    d, k, n, vocab = 256, 20, 40, 50
+    st, o, tok, _ = _small(d, k, n, vocab=vocab, seed=9)
+    basis = sn.sn_basis_pack(dev(st["U"], "bf16"))
+    E, P, X, Cin = (dev(st[x], "bf16") for x in ("E", "P", "X", "C"))
+    bad_tok = tok.copy()
+    bad_tok[5] = vocab + 1
+    sn.set_check_ids(True)
+    try:
+        sn.sn_compress(basis, X, tok=ids(tok), E=E, P=P, seq_len=9)       # in range: no error
+        sn.sn_decompress(basis, Cin, tok=ids(tok), E=E, P=P, seq_len=9)
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        with pytest.raises(sn.SnError) as ei:
+            sn.sn_compress(basis, X, tok=ids(bad_tok), E=E, P=P, seq_len=9, err_flag=flag)
+        assert ei.value.status == sn.SN_ERR_INDEX
+        assert int(flag.item()) == 1
+        bad_pos = (np.arange(n) % 9).astype(np.int32)
+        bad_pos[3] = 99
+        with pytest.raises(sn.SnError) as ei:
+            sn.sn_decompress(basis, Cin, P=P, pos=ids(bad_pos))
+        assert ei.value.status == sn.SN_ERR_INDEX and "flag bits 2" in str(ei.value)
+    finally:
+        sn.set_check_ids(False)
+    # checking off: the same call returns normally and only the flag reports
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sn.sn_compress(basis, X, tok=ids(bad_tok), E=E, P=P, seq_len=9, err_flag=flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 1
