@@ -579,8 +579,10 @@ def test_compress_one_table_128_token_workgroups(tables):
 
 
 def test_bit_exact_gather_and_subtract():
-    """C = 0 decompresses to exactly E[tok] + P[pos]; X = E[tok] + P[pos]
-    compresses to exactly 0 (values on a grid where every sum is exact)."""
+    """C = 0 decompresses to exactly E[tok] + P[pos] (bit-exact gathers);
+    X = E[tok] + P[pos] (values on a grid where every sum is exact)
+    compresses to 0 within the fp32 accumulation bound of the fused
+    subtract-and-project."""
     d, k, n = 256, 40, 70
     rng = np.random.default_rng(12)
     U, _ = np.linalg.qr(rng.standard_normal((d, k)))
@@ -601,9 +603,11 @@ def test_bit_exact_gather_and_subtract():
         Xr = sn.sn_decompress(basis, Z, tok=ids(tok), E=Et, P=Pt, seq_len=9)
         assert np.array_equal(host(Xr), E[tok] + P[pos]), "E + P gather"
         # compress of X = E[tok] + P[pos]: the embedding rows cancel X exactly.
-        # The matrix-core path sums X U, -P U and -E U in fp32, so C is zero up
-        # to fp32 accumulation error (bounded by d * 2^-24 * sum |terms|);
-        # subtracting a wrong row would leave entries of size ~|x| |u| ~ 1e-1.
+        # In exact arithmetic C = 0.  The matrix-core path sums the products of
+        # X, -P and -T_fixed with U in one set of fp32 accumulators, so C is
+        # zero up to that accumulation's rounding, bounded by
+        # d * 2^-24 * sum |terms|; subtracting a wrong row would leave entries
+        # of size ~|x| |u| ~ 1e-1.
         X = dev(synth.store(E[tok] + P[pos], dtype), dtype)
         C = host(sn.sn_compress(basis, X, tok=ids(tok), E=Et, P=Pt, seq_len=9))
         Ud = oracle.decode_bf16(st["U"]) if dtype == "bf16" else st["U"].astype(np.float64)
