@@ -1089,7 +1089,11 @@ def main():
         "value_is": "codec_pair: compress + decompress back to back (algorithmic bytes of the "
                     "pair / pair time); the whole step (all hot-path ops) is under 'step'",
         "frac_hbm": round(pair_gbs / HBM_PEAK_GBS, 4),
+        "frac_is": "algorithmic bytes of the pair / pair time / 8 TB/s (gathered rows largely "
+                   "served by the Infinity Cache in the back-to-back loop); cold_GBps is the same "
+                   "pair after a 512 MB flush",
         "cold_GBps": round(rate(pair_bytes, cold_ms), 1),
+        "cold_frac_hbm": round(rate(pair_bytes, cold_ms) / HBM_PEAK_GBS, 4),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
