@@ -616,6 +616,30 @@ def test_bit_exact_gather_and_subtract():
         log(f"  bit-exact gather, cancelling subtract ok ({dtype}); max |C| {np.abs(C).max():.3g}")
 
 
+def test_decompress_cancelling_tables():
+    """P[pos] = -T_fixed[tok] for every token: the tables cancel exactly and
+    X' is C U^T alone, although each table entry is ~64 times the result.
+    The sum of three addends must keep the small one (Sec. 4.3.1 recovery)."""
+    d, k, seq, batch = 512, 40, 64, 4
+    n = seq * batch
+    rng = np.random.default_rng(31)
+    U, _ = np.linalg.qr(rng.standard_normal((d, k)))
+    E = rng.integers(-4096, 4096, (seq, d)) / 64.0
+    P = -E
+    tok = (np.arange(n) % seq).astype(np.int32)
+    Cin = rng.standard_normal((n, k))
+    for dtype in ("bf16", "f32"):
+        st = {nm: synth.store(a, dtype) for nm, a in dict(U=U, E=E, P=P, C=Cin).items()}
+        basis = sn.sn_basis_pack(dev(st["U"], dtype))
+        Xr = host(sn.sn_decompress(basis, dev(st["C"], dtype), tok=ids(tok),
+                                   E=dev(st["E"], dtype), P=dev(st["P"], dtype), seq_len=seq))
+        val = (lambda a: oracle.decode_bf16(a)) if dtype == "bf16" else (
+            lambda a: a.astype(np.float64))
+        ref = oracle.decompress(val(st["C"]), val(st["U"]), tok=tok, E=val(st["E"]),
+                                P=val(st["P"]), seq_len=seq)
+        assert_parity(Xr, ref, dtype, f"decompress, cancelling tables ({dtype})")
+
+
 def test_output_rounding_ties_to_even():
     """Outputs are rounded once, to nearest even: 1 + 2^-8 -> 1, 1 + 3*2^-8 -> 1 + 2^-6."""
     d, k = 64, 8
