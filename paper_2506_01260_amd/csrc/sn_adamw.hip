@@ -13,11 +13,14 @@
 // App. A): no projection is needed for W_p2.
 //
 // Memory-bound.  A thread owns 8 consecutive columns (16-byte loads of bf16
-// G / W, 32-byte loads of M and V) over kRows rows.  Standard: one pass
-// (22 bytes per bf16 element).  Subspace: pass 1 updates V and writes
-// per-block column sums of it; pass 2 adds the blocks in a fixed order and
-// forms alpha; pass 3 reads G again, updates M and W (24 bytes per element:
-// G is read twice, M once).
+// G / W, 32-byte loads of M and V) over a few rows; the loads of many waves
+// in flight, not the work per thread, set the speed.  Standard: one pass
+// (22 bytes per bf16 element), 256 column threads x 4 rows per workgroup.
+// Subspace: pass 1 updates V and writes per-block column sums of it (a
+// workgroup is 64 column threads x 4 row groups of 8 rows, its 32-row column
+// sums added across the row groups in LDS in a fixed order); pass 2 adds the
+// blocks in a fixed order and forms alpha; pass 3 reads G again, updates M
+// and W (24 bytes per element: G is read twice, M once).
 #include "sn_device.h"
 #include "sn_internal.h"
 
@@ -25,9 +28,12 @@ namespace sn {
 
 namespace {
 
-constexpr int kRows = 32;     // rows per thread
 constexpr int kCols = 8;      // columns per thread
-constexpr int kBlock = 128;   // threads per workgroup (1024 columns)
+// workgroup geometry: column threads x row groups, rows per thread
+constexpr int kStdCT = 256, kStdRG = 1, kStdR = 4;  // standard step
+constexpr int kSubCT = 64, kSubRG = 4, kSubR = 8;   // subspace step (32-row blocks)
+constexpr int kSubRows = kSubRG * kSubR;            // rows per column-sum block
+constexpr int kAlphaBlock = 128;
 
 struct AdamArgs {
   float b1, omb1, b2, omb2;   // beta1, 1 - beta1, beta2, 1 - beta2
@@ -89,21 +95,23 @@ __device__ __forceinline__ void store8(T *row, int64_t c0, int64_t cols, const f
 
 // Pass 1 (and the whole standard step when !SUB): the second moment and
 // either its column sums (SUB) or the first moment and the W update with the
-// entrywise rate.
-template <typename T, bool VEC, bool SUB>
-__global__ __launch_bounds__(kBlock) void moments_kernel(T *__restrict__ W, int64_t ldw,
-                                                         const T *__restrict__ G, int64_t ldg,
-                                                         float *__restrict__ M,
-                                                         float *__restrict__ V, int64_t ldm,
-                                                         int64_t rows, int64_t cols, AdamArgs a,
-                                                         float *__restrict__ colsum) {
-  const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kCols;
-  if (c0 >= cols) return;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kRows;
-  const int64_t r1 = r0 + kRows < rows ? r0 + kRows : rows;
+// entrywise rate.  Thread (x, y) of the workgroup: columns 8 x .. 8 x + 7 of
+// the workgroup's column block, rows R y .. R y + R - 1 of its row block.
+template <typename T, bool VEC, bool SUB, int CT, int RG, int R>
+__global__ __launch_bounds__(CT * RG) void moments_kernel(T *__restrict__ W, int64_t ldw,
+                                                           const T *__restrict__ G, int64_t ldg,
+                                                           float *__restrict__ M,
+                                                           float *__restrict__ V, int64_t ldm,
+                                                           int64_t rows, int64_t cols, AdamArgs a,
+                                                           float *__restrict__ colsum) {
+  __shared__ float red[SUB ? RG : 1][SUB ? CT * kCols : 1];
+  const int tx = threadIdx.x % CT, ty = threadIdx.x / CT;
+  const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * CT + tx) * kCols;
+  const bool live = c0 < cols;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * (RG * R) + ty * R;
+  const int64_t r1 = !live ? r0 : (r0 + R < rows ? r0 + R : (r0 < rows ? rows : r0));
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int64_t r = r0; r < r1; ++r) {
+  auto row = [&](int64_t r) {
     float g[8], v[8];
     load8<T, VEC>(G + r * ldg, c0, cols, g);
     load8<float, VEC>(V + r * ldm, c0, cols, v);
@@ -127,22 +135,43 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(T *__restrict__ W, int6
       }
       store8<T, VEC>(W + r * ldw, c0, cols, w);
     }
+  };
+  // a full run of R rows is unrolled as one block (all its loads in flight
+  // together); a short run at the bottom edge goes row by row
+  if (r1 - r0 == R) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) row(r0 + j);
+  } else {
+    for (int64_t r = r0; r < r1; ++r) row(r);
   }
   if constexpr (SUB) {
-    float *dst = colsum + static_cast<int64_t>(blockIdx.y) * cols;
+    // the row groups' sums of each column, added in row order
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (c0 + i < cols) dst[c0 + i] = s[i];
+    for (int i = 0; i < 8; ++i) red[ty][tx * kCols + i] = s[i];
+    __syncthreads();
+    if (ty == 0 && live) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float t = red[0][tx * kCols + i];
+#pragma unroll
+        for (int y = 1; y < RG; ++y) t += red[y][tx * kCols + i];
+        s[i] = t;
+      }
+      float *dst = colsum + static_cast<int64_t>(blockIdx.y) * cols;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (c0 + i < cols) dst[c0 + i] = s[i];
+    }
   }
 }
 
 // Pass 2: alpha_c = 1 / (sqrt(sum_blocks colsum / (rows (1 - b2^t))) + eps),
 // the row blocks added in a fixed order in float64.
-__global__ __launch_bounds__(kBlock) void alpha_kernel(const float *__restrict__ colsum,
+__global__ __launch_bounds__(kAlphaBlock) void alpha_kernel(const float *__restrict__ colsum,
                                                        int64_t nblk, int64_t rows, int64_t cols,
                                                        double inv_bc2, double eps,
                                                        float *__restrict__ alpha) {
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * kAlphaBlock + threadIdx.x;
   if (c >= cols) return;
   double s = 0.0;
 #pragma unroll 4
@@ -152,23 +181,23 @@ __global__ __launch_bounds__(kBlock) void alpha_kernel(const float *__restrict__
 }
 
 // Pass 3: M <- b1 M + (1 - b1) G, then W <- W - lr alpha_c M^ - wd W with
-// the column's rate.
-template <typename T, bool VEC>
-__global__ __launch_bounds__(kBlock) void apply_kernel(T *__restrict__ W, int64_t ldw,
-                                                       const T *__restrict__ G, int64_t ldg,
-                                                       float *__restrict__ M, int64_t ldm,
-                                                       int64_t rows, int64_t cols, AdamArgs a,
-                                                       const float *__restrict__ alpha) {
-  const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kCols;
+// the column's rate (the geometry of pass 1).
+template <typename T, bool VEC, int CT, int RG, int R>
+__global__ __launch_bounds__(CT * RG) void apply_kernel(T *__restrict__ W, int64_t ldw,
+                                                         const T *__restrict__ G, int64_t ldg,
+                                                         float *__restrict__ M, int64_t ldm,
+                                                         int64_t rows, int64_t cols, AdamArgs a,
+                                                         const float *__restrict__ alpha) {
+  const int tx = threadIdx.x % CT, ty = threadIdx.x / CT;
+  const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * CT + tx) * kCols;
   if (c0 >= cols) return;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kRows;
-  const int64_t r1 = r0 + kRows < rows ? r0 + kRows : rows;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * (RG * R) + ty * R;
+  const int64_t r1 = r0 + R < rows ? r0 + R : (r0 < rows ? rows : r0);
   float al[8];
   load8<float, VEC>(alpha, c0, cols, al);
 #pragma unroll
   for (int i = 0; i < 8; ++i) al[i] *= a.lr * a.inv_bc1;
-#pragma unroll 4
-  for (int64_t r = r0; r < r1; ++r) {
+  auto row = [&](int64_t r) {
     float g[8], m[8], w[8];
     load8<T, VEC>(G + r * ldg, c0, cols, g);
     load8<float, VEC>(M + r * ldm, c0, cols, m);
@@ -180,6 +209,12 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(T *__restrict__ W, int64_
     }
     store8<float, VEC>(M + r * ldm, c0, cols, m);
     store8<T, VEC>(W + r * ldw, c0, cols, w);
+  };
+  if (r1 - r0 == R) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) row(r0 + j);
+  } else {
+    for (int64_t r = r0; r < r1; ++r) row(r);
   }
 }
 
@@ -189,20 +224,23 @@ hipError_t launch_t(void *Wv, int64_t ldw, const void *Gv, int64_t ldg, float *M
                     double eps, bool sub, void *ws, hipStream_t s) {
   T *W = static_cast<T *>(Wv);
   const T *G = static_cast<const T *>(Gv);
-  const dim3 grid(static_cast<unsigned>(ceil_div(cols, kBlock * kCols)),
-                  static_cast<unsigned>(ceil_div(rows, kRows)));
   if (!sub) {
-    moments_kernel<T, VEC, false><<<grid, kBlock, 0, s>>>(W, ldw, G, ldg, M, V, ldm, rows, cols,
-                                                          a, nullptr);
+    const dim3 grid(static_cast<unsigned>(ceil_div(cols, kStdCT * kCols)),
+                    static_cast<unsigned>(ceil_div(rows, kStdRG * kStdR)));
+    moments_kernel<T, VEC, false, kStdCT, kStdRG, kStdR><<<grid, kStdCT * kStdRG, 0, s>>>(
+        W, ldw, G, ldg, M, V, ldm, rows, cols, a, nullptr);
     return hipGetLastError();
   }
+  const dim3 grid(static_cast<unsigned>(ceil_div(cols, kSubCT * kCols)),
+                  static_cast<unsigned>(ceil_div(rows, kSubRows)));
   float *colsum = static_cast<float *>(ws);
   float *alpha = colsum + static_cast<int64_t>(grid.y) * cols;
-  moments_kernel<T, VEC, true><<<grid, kBlock, 0, s>>>(W, ldw, G, ldg, M, V, ldm, rows, cols, a,
-                                                       colsum);
-  alpha_kernel<<<dim3(static_cast<unsigned>(ceil_div(cols, kBlock))), kBlock, 0, s>>>(
+  moments_kernel<T, VEC, true, kSubCT, kSubRG, kSubR><<<grid, kSubCT * kSubRG, 0, s>>>(
+      W, ldw, G, ldg, M, V, ldm, rows, cols, a, colsum);
+  alpha_kernel<<<dim3(static_cast<unsigned>(ceil_div(cols, kAlphaBlock))), kAlphaBlock, 0, s>>>(
       colsum, grid.y, rows, cols, inv_bc2, eps, alpha);
-  apply_kernel<T, VEC><<<grid, kBlock, 0, s>>>(W, ldw, G, ldg, M, ldm, rows, cols, a, alpha);
+  apply_kernel<T, VEC, kSubCT, kSubRG, kSubR><<<grid, kSubCT * kSubRG, 0, s>>>(
+      W, ldw, G, ldg, M, ldm, rows, cols, a, alpha);
   return hipGetLastError();
 }
 
@@ -211,8 +249,8 @@ bool a16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 }  // namespace
 
 size_t adamw_workspace_bytes(int64_t rows, int64_t cols) {
-  // column sums per block of kRows rows, then the rates (fp32)
-  return align256(static_cast<size_t>(ceil_div(rows, kRows) + 1) * cols * sizeof(float));
+  // column sums per block of kSubRows rows, then the rates (fp32)
+  return align256(static_cast<size_t>(ceil_div(rows, kSubRows) + 1) * cols * sizeof(float));
 }
 
 hipError_t launch_adamw(int dt, void *W, int64_t ldw, const void *G, int64_t ldg, float *M,
