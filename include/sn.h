@@ -383,8 +383,9 @@ int32_t sn_embed_lowrank_forward(const void *basis, int64_t d, int64_t k, int32_
  *   gCS   vocab x k float32 gradient, row stride ldgc >= k, ACCUMULATED into
  *         (rows of ids that do not occur are untouched)
  *   workspace  sn_embed_lowrank_workspace_bytes(d, k, dt, N, vocab) bytes
- * Deterministic: the rows of each id are summed in ascending token order in
- * float64 (after a stable counting sort of the token indices by id).  Errors:
+ * Deterministic: the rows of each id are summed in float64 in a fixed order:
+ * ascending token order within each block of 512 tokens (a stable sort of the
+ * block's tokens by id), then the blocks in ascending order.  Errors:
  * NULL, SHAPE, DTYPE, ALIGN, ALIAS, WORKSPACE, UNSUPPORTED, HIP. */
 int32_t sn_embed_lowrank_backward(const void *basis, int64_t d, int64_t k, int32_t dt,
                                   const void *dX0, int64_t N, int64_t ldg, const int32_t *tok,

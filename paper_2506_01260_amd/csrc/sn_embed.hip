@@ -8,13 +8,11 @@
 //           recovery with C = C_S[tok]).
 // backward  gC_S[v] += sum over i with tok_i = v of dX0[i] U: the gradient
 //           coefficients dX0 U in fp32 (the compress kernel's fp32-row
-//           epilogue), then a deterministic segmented sum by token id: a
-//           stable counting sort of the token indices (per-block id
-//           histograms, per-id prefixes over the blocks, one scan over the
-//           vocabulary, and a bitonic sort of each block's (id, index) keys
-//           in LDS for the ranks within a block), per-chunk sums of at most
-//           64 rows of a segment, and per-segment sums of its chunks, every
-//           sum in a fixed order in float64.
+//           epilogue), then a deterministic sum by token id in two kernels:
+//           per block of 512 tokens, a bitonic sort of the (id, index) keys
+//           in LDS and, per run of equal ids, the float64 sum of its rows in
+//           ascending token order; per id, the sum of its runs over the
+//           blocks in block order (float64), added to gC_S.
 #include "sn_device.h"
 #include "sn_internal.h"
 
@@ -22,16 +20,13 @@ namespace sn {
 
 namespace {
 
-constexpr int kSortThreads = 1024;
-
-__device__ __forceinline__ int64_t ceil_div_dev(int64_t a, int64_t b) { return (a + b - 1) / b; }
-constexpr int kChunk = 64;  // rows per chunk of a segment
+constexpr int kBlk = 512;      // tokens per sort block (threads of block_runs_kernel)
+constexpr int kBlkWaves = kBlk / 64;
+constexpr int kIdRange = 64;   // ids per workgroup of id_merge_kernel
 
 struct EmbedPlan {
-  int64_t kp = 0, maxseg = 0, maxchunk = 0, nblk = 0, ntile = 0;
-  size_t off_lz = 0, off_lch = 0, off_tiles = 0, off_count = 0;
-  size_t off_c = 0, off_cnt = 0, off_cur = 0, off_order = 0, off_segid = 0, off_segoff = 0,
-         off_segch = 0, off_cbeg = 0, off_cend = 0, off_meta = 0, off_part = 0, total = 0;
+  int64_t kp = 0, nblk = 0, nq = 0;
+  size_t off_c = 0, off_rid = 0, off_first = 0, off_part = 0, total = 0;
 };
 
 EmbedPlan embed_plan(int64_t k, int dt, int64_t N, int64_t vocab, bool backward) {
@@ -47,29 +42,14 @@ EmbedPlan embed_plan(int64_t k, int dt, int64_t N, int64_t vocab, bool backward)
     P.total = off;
     return P;
   }
-  P.maxseg = N < vocab ? N : vocab;
-  P.maxchunk = ceil_div(N, kChunk) + P.maxseg;
-  P.nblk = ceil_div(N, kSortThreads);
-  auto ints = [&](size_t &o, int64_t n) {
-    o = off;
-    off = align256(off + static_cast<size_t>(n) * 4);
-  };
-  ints(P.off_cnt, P.nblk * vocab);  // per-block id counts, then their prefixes over blocks
-  ints(P.off_cur, vocab);           // per-id totals, then the ids' first slots
-  P.ntile = ceil_div(vocab, kSortThreads);
-  ints(P.off_count, vocab);         // per-id token counts
-  ints(P.off_lz, vocab);            // per id: segments and chunks before it in its tile
-  ints(P.off_lch, vocab);
-  ints(P.off_tiles, 6 * P.ntile);   // per tile: tokens, segments, chunks; then their offsets
-  ints(P.off_order, N);
-  ints(P.off_segid, P.maxseg);
-  ints(P.off_segoff, P.maxseg + 1);
-  ints(P.off_segch, P.maxseg + 1);
-  ints(P.off_cbeg, P.maxchunk);
-  ints(P.off_cend, P.maxchunk);
-  ints(P.off_meta, 4);
-  P.off_part = off;
-  off = align256(off + static_cast<size_t>(P.maxchunk) * P.kp * 8);
+  P.nblk = ceil_div(N, kBlk);
+  P.nq = ceil_div(vocab, kIdRange);
+  P.off_rid = off;  // per block: the ids of its runs, ascending
+  off = align256(off + static_cast<size_t>(P.nblk) * kBlk * 4);
+  P.off_first = off;  // per block: the first run of each range of kIdRange ids, then the runs
+  off = align256(off + static_cast<size_t>(P.nblk) * (P.nq + 1) * 4);
+  P.off_part = off;  // per block and run: the float64 sum of the run's rows
+  off = align256(off + static_cast<size_t>(P.nblk) * kBlk * P.kp * 8);
   P.total = off;
   return P;
 }
@@ -92,20 +72,20 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T *__restrict__ 
   C[idx] = CS[v * ldcs + j];
 }
 
-// Exclusive scan of one int per thread over the 1024 threads (Hillis-Steele
+// Exclusive scan of one int per thread over the block's threads (Hillis-Steele
 // in LDS); *total receives the sum.
 __device__ int block_excl_scan(int v, int *buf, int *total) {
   const int t = threadIdx.x;
   buf[t] = v;
   __syncthreads();
-  for (int off = 1; off < kSortThreads; off <<= 1) {
+  for (int off = 1; off < kBlk; off <<= 1) {
     const int add = t >= off ? buf[t - off] : 0;
     __syncthreads();
     buf[t] += add;
     __syncthreads();
   }
   const int incl = buf[t];
-  *total = buf[kSortThreads - 1];
+  *total = buf[kBlk - 1];
   __syncthreads();
   return incl - v;
 }
@@ -120,138 +100,33 @@ __device__ __forceinline__ int clamp_tok(const int32_t *tok, int64_t i, int64_t 
   return static_cast<int>(v);
 }
 
-// cnt[b][v] = number of tokens of block b (1024 tokens each) with id v; the
-// block clears its own row first (the barrier orders the clearing stores
-// before the block's increments)
-__global__ __launch_bounds__(kSortThreads) void hist_kernel(const int32_t *__restrict__ tok,
-                                                            int64_t N, int64_t vocab,
-                                                            int32_t *err_flag,
-                                                            int32_t *__restrict__ cnt) {
-  int32_t *row = cnt + static_cast<int64_t>(blockIdx.x) * vocab;
-  for (int64_t v = threadIdx.x; v < vocab; v += kSortThreads) row[v] = 0;
-  __syncthreads();
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
-  if (i < N) atomicAdd(&row[clamp_tok(tok, i, vocab, err_flag)], 1);
-}
-
-// per id v: cnt[b][v] <- tokens of id v in the blocks before b; tot[v] <- all of them
-__global__ __launch_bounds__(256) void block_prefix_kernel(int32_t *__restrict__ cnt,
-                                                           int64_t nblk, int64_t vocab,
-                                                           int32_t *__restrict__ tot,
-                                                           int32_t *__restrict__ count) {
-  const int64_t v = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (v >= vocab) return;
-  int run = 0;
-  for (int64_t b = 0; b < nblk; ++b) {
-    const int c = cnt[b * vocab + v];
-    cnt[b * vocab + v] = run;
-    run += c;
-  }
-  tot[v] = run;
-  count[v] = run;
-}
-
-// Scan over the vocabulary in three kernels.  Tile pass: per 1024-id tile,
-// exclusive prefixes within the tile of the ids' token counts, of the ids
-// that occur (segments) and of their chunks (at most kChunk rows each), and
-// the tile's three totals.
-__global__ __launch_bounds__(kSortThreads) void tile_scan_kernel(
-    int64_t vocab, int32_t *__restrict__ tot, int32_t *__restrict__ lz,
-    int32_t *__restrict__ lch, int32_t *__restrict__ tiles, int64_t ntile) {
-  __shared__ int buf[kSortThreads];
-  const int64_t v = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
-  const int c = v < vocab ? tot[v] : 0;
-  int sc, sz, sch;
-  const int ec = block_excl_scan(c, buf, &sc);
-  const int ez = block_excl_scan(c > 0, buf, &sz);
-  const int ech = block_excl_scan((c + kChunk - 1) / kChunk, buf, &sch);
-  if (v < vocab) {
-    tot[v] = ec;
-    lz[v] = ez;
-    lch[v] = ech;
-  }
-  if (threadIdx.x == 0) {
-    tiles[blockIdx.x] = sc;
-    tiles[ntile + blockIdx.x] = sz;
-    tiles[2 * ntile + blockIdx.x] = sch;
-  }
-}
-
-// One workgroup: exclusive prefixes of the tiles' totals (into tiles[3 ntile
-// ..]), the segment and chunk counts, and the end markers of both tables.
-__global__ __launch_bounds__(kSortThreads) void tiles_scan_kernel(
-    int64_t N, int32_t *__restrict__ tiles, int64_t ntile, int32_t *__restrict__ seg_off,
-    int32_t *__restrict__ seg_ch, int32_t *__restrict__ meta) {
-  __shared__ int buf[kSortThreads];
-  const int64_t per = ceil_div_dev(ntile, kSortThreads);
-  const int64_t t0 = threadIdx.x * per < ntile ? threadIdx.x * per : ntile;
-  const int64_t t1 = t0 + per < ntile ? t0 + per : ntile;
-  for (int a = 0; a < 3; ++a) {
-    int sum = 0;
-    for (int64_t i = t0; i < t1; ++i) sum += tiles[a * ntile + i];
-    int total;
-    int run = block_excl_scan(sum, buf, &total);
-    for (int64_t i = t0; i < t1; ++i) {
-      const int c = tiles[a * ntile + i];
-      tiles[(3 + a) * ntile + i] = run;
-      run += c;
-    }
-    if (threadIdx.x == 0 && a == 1) meta[0] = total;
-    if (threadIdx.x == 0 && a == 2) meta[1] = total;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    seg_off[meta[0]] = static_cast<int>(N);
-    seg_ch[meta[0]] = meta[1];
-  }
-}
-
-// Per id: its first slot, and for an id that occurs its segment entry and
-// chunk table entries.
-__global__ __launch_bounds__(kSortThreads) void tile_write_kernel(
-    int64_t vocab, const int32_t *__restrict__ cnt_last, int64_t nblk, int32_t *__restrict__ tot,
-    const int32_t *__restrict__ lz, const int32_t *__restrict__ lch,
-    const int32_t *__restrict__ tiles, int64_t ntile, int32_t *__restrict__ seg_id,
-    int32_t *__restrict__ seg_off, int32_t *__restrict__ seg_ch, int32_t *__restrict__ cbeg,
-    int32_t *__restrict__ cend, const int32_t *__restrict__ count) {
-  const int64_t tile = blockIdx.x;
-  const int64_t v = tile * kSortThreads + threadIdx.x;
-  if (v >= vocab) return;
-  const int first = tiles[3 * ntile + tile] + tot[v];
-  tot[v] = first;
-  const int c = count[v];
-  if (c == 0) return;
-  const int sgi = tiles[4 * ntile + tile] + lz[v];
-  int q = tiles[5 * ntile + tile] + lch[v];
-  seg_id[sgi] = static_cast<int>(v);
-  seg_off[sgi] = first;
-  seg_ch[sgi] = q;
-  for (int b = 0; b < c; b += kChunk, ++q) {
-    cbeg[q] = first + b;
-    cend[q] = first + (b + kChunk < c ? b + kChunk : c);
-  }
-  (void)cnt_last;
-  (void)nblk;
-}
-
-// Block b's tokens in sorted order: keys (id << 10 | local index) sorted in
-// LDS (bitonic), a token's rank among the block's tokens of its id is its
-// sorted position minus the first position of its id (a max scan of the run
-// heads), and its slot is first[id] + (id's tokens in earlier blocks) + rank.
-// Ids must be below 2^21.
-__global__ __launch_bounds__(kSortThreads) void place_kernel(
-    const int32_t *__restrict__ tok, int64_t N, int64_t vocab, const int32_t *__restrict__ cnt,
-    const int32_t *__restrict__ first, int32_t *__restrict__ order) {
-  __shared__ uint32_t key[kSortThreads];
-  __shared__ int hs[kSortThreads];
+// Block b (tokens base .. base + 511): the keys (id << 9 | local index)
+// sorted in LDS (bitonic), so each run of equal ids lists its tokens in
+// ascending order.  rid[b][r] = the id of run r (ascending); first[b][q] =
+// the first run with an id of at least q kIdRange (q = 0 .. nq, first[b][nq]
+// = the runs); part[b][r][:] = the float64 sum of the run's c32 rows in
+// order.  Wave w sums the sorted positions 64 w .. 64 w + 63 (lane = column,
+// 64 columns per pass): a run that begins and ends inside the wave is written
+// directly; a run that crosses waves leaves its first and middle pieces in
+// LDS and the wave where it ends adds them in order.  Ids must be below 2^21.
+__global__ __launch_bounds__(kBlk) void block_runs_kernel(
+    const int32_t *__restrict__ tok, int64_t N, int64_t vocab, int32_t *err_flag,
+    const float *__restrict__ c32, int kp, int64_t nq, int32_t *__restrict__ rid_out,
+    int32_t *__restrict__ first, double *__restrict__ part) {
+  __shared__ uint32_t key[kBlk];
+  __shared__ int rid[kBlk + 1];     // run of each sorted position (-1 past the end)
+  __shared__ int rstart[kBlk + 1];  // first sorted position of each run
+  __shared__ int runid[kBlk];       // id of each run
+  __shared__ int buf[kBlk];
+  __shared__ double piece[kBlkWaves][64];  // a wave's unfinished last run
   const int t = threadIdx.x;
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortThreads;
-  const int64_t i = base + t;
-  key[t] = i < N ? (static_cast<uint32_t>(clamp_tok(tok, i, vocab, nullptr)) << 10) |
-                       static_cast<uint32_t>(t)
-                 : 0xFFFFFFFFu;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kBlk;
+  const int nvalid = N - base < kBlk ? static_cast<int>(N - base) : kBlk;
+  key[t] = t < nvalid ? (static_cast<uint32_t>(clamp_tok(tok, base + t, vocab, err_flag)) << 9) |
+                            static_cast<uint32_t>(t)
+                      : 0xFFFFFFFFu;
   __syncthreads();
-  for (int kk = 2; kk <= kSortThreads; kk <<= 1) {
+  for (int kk = 2; kk <= kBlk; kk <<= 1) {
     for (int j = kk >> 1; j > 0; j >>= 1) {
       const int p = t ^ j;
       if (p > t) {
@@ -265,70 +140,148 @@ __global__ __launch_bounds__(kSortThreads) void place_kernel(
     }
   }
   const uint32_t me = key[t];
-  const bool head = t == 0 || (key[t - 1] >> 10) != (me >> 10);
-  hs[t] = head ? t : 0;
+  const bool head = t < nvalid && (t == 0 || (key[t - 1] >> 9) != (me >> 9));
+  int nrun = 0;
+  const int before = block_excl_scan(head ? 1 : 0, buf, &nrun);
+  rid[t] = t < nvalid ? (head ? before : before - 1) : -1;
+  if (head) {
+    rstart[before] = t;
+    runid[before] = static_cast<int>(me >> 9);
+    rid_out[base + before] = static_cast<int32_t>(me >> 9);
+  }
+  if (t == 0) {
+    rid[kBlk] = -1;
+    rstart[nrun] = nvalid;
+  }
   __syncthreads();
-  for (int off = 1; off < kSortThreads; off <<= 1) {  // inclusive max scan
-    const int o = t >= off ? hs[t - off] : 0;
-    __syncthreads();
-    hs[t] = hs[t] > o ? hs[t] : o;
-    __syncthreads();
+  {  // the range index: run r is the first of the ranges after its predecessor's
+    int32_t *fb = first + static_cast<int64_t>(blockIdx.x) * (nq + 1);
+    if (t < nrun) {
+      const int64_t q1 = runid[t] / kIdRange;
+      const int64_t q0 = t == 0 ? 0 : runid[t - 1] / kIdRange + 1;
+      for (int64_t q = q0; q <= q1; ++q) fb[q] = t;
+      if (t == nrun - 1)
+        for (int64_t q = q1 + 1; q <= nq; ++q) fb[q] = nrun;
+    }
   }
-  if (me != 0xFFFFFFFFu) {
-    const int64_t id = me >> 10;
-    const int rank = t - hs[t];
-    const int64_t slot = first[id] + cnt[static_cast<int64_t>(blockIdx.x) * vocab + id] + rank;
-    order[slot] = static_cast<int32_t>(base + (me & 1023u));
+
+  const int w = t >> 6, lane = t & 63;
+  const int p0 = 64 * w;
+  for (int j0 = 0; j0 < kp; j0 += 64) {  // the same trip count in every wave
+    const int j = j0 + lane;
+    const bool col = j < kp;
+    const int jc = col ? j : kp - 1;
+    // every load is issued (positions past the end read the last token's row)
+    float v[64];
+#pragma unroll
+    for (int s2 = 0; s2 < 64; ++s2) {
+      const int p = p0 + s2 < nvalid ? p0 + s2 : nvalid - 1;
+      v[s2] = c32[(base + (key[p] & 511u)) * kp + jc];
+    }
+    // lane L describes position p0 + L: whether a run ends there (and its
+    // run); the sequential sum below reads them as scalars
+    const int pl = p0 + lane;
+    const int rl = pl < nvalid ? rid[pl] : -1;
+    const uint64_t ends = __ballot(pl < nvalid && rid[pl + 1] != rl);
+    const uint64_t valid = __ballot(pl < nvalid);
+    const int first_run = __shfl(rl, 0, 64);
+    const bool first_open = nvalid > p0 && rstart[first_run > 0 ? first_run : 0] < p0;
+    double acc = 0.0, tail = 0.0;
+    int tail_run = -1;
+    bool open = first_open;  // the current run began in an earlier wave
+#pragma unroll
+    for (int s2 = 0; s2 < 64; ++s2) {
+      if ((valid >> s2) & 1) {
+        acc += static_cast<double>(v[s2]);
+        if ((ends >> s2) & 1) {  // the run ends here
+          const int r = __builtin_amdgcn_readlane(rl, s2);
+          if (!open) {
+            if (col) part[((base + r) * kp) + j] = acc;
+          } else {  // begun in an earlier wave: finished below
+            tail = acc;
+            tail_run = r;
+          }
+          acc = 0.0;
+          open = false;
+        } else if (s2 == 63) {  // continues into the next wave
+          piece[w][lane] = acc;
+        }
+      }
+    }
+    __syncthreads();
+    if (tail_run >= 0) {
+      double tot = 0.0;
+      for (int w2 = rstart[tail_run] >> 6; w2 < w; ++w2) tot += piece[w2][lane];
+      tot += tail;
+      if (col) part[((base + tail_run) * kp) + j] = tot;
+    }
+    __syncthreads();
   }
 }
 
-// One wave per chunk: part[q][j] = sum over the chunk's rows (ascending
-// token index) of c32[row][j], float64.  Lane r copies row r of the chunk
-// into LDS (contiguous loads), then lane j adds column j down the rows.
-__global__ __launch_bounds__(256) void chunk_sum_kernel(const float *__restrict__ c32, int64_t kp,
-                                                        const int32_t *__restrict__ order,
-                                                        const int32_t *__restrict__ cbeg,
-                                                        const int32_t *__restrict__ cend,
-                                                        const int32_t *__restrict__ meta,
-                                                        double *__restrict__ part) {
-  constexpr int JC = 64, LD = JC + 1;  // columns per pass, LDS row stride
-  __shared__ float rows[4][kChunk * LD];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + w;
-  const bool live = q < meta[1];
-  const int b = live ? cbeg[q] : 0, len = live ? cend[q] - b : 0;
-  float *rw = rows[w];
-  for (int64_t j0 = 0; j0 < kp; j0 += JC) {  // same trip count in every wave
-    const int64_t jn = kp - j0 < JC ? kp - j0 : JC;
-    if (lane < len) {
-      const float *src = c32 + static_cast<int64_t>(order[b + lane]) * kp + j0;
-      for (int64_t j = 0; j < jn; ++j) rw[lane * LD + j] = src[j];
-    }
-    __syncthreads();
-    if (live && lane < jn) {
-      double acc = 0.0;
-      for (int r = 0; r < len; ++r) acc += static_cast<double>(rw[r * LD + lane]);
-      part[q * kp + j0 + lane] = acc;
-    }
-    __syncthreads();
-  }
-}
-
-// One wave per segment: gCS[v][j] += the segment's chunk sums, in order.
-__global__ __launch_bounds__(256) void seg_sum_kernel(const double *__restrict__ part, int64_t kp,
-                                                      int64_t k, const int32_t *__restrict__ seg_id,
-                                                      const int32_t *__restrict__ seg_ch,
-                                                      const int32_t *__restrict__ meta,
-                                                      float *__restrict__ gCS, int64_t ldgc) {
+// One wave per id v: lane L takes block c0 + L (64 blocks per pass) and finds
+// the block's run of id v through the range index (first[b][v / kIdRange]
+// ..); the blocks that hold v are then visited in ascending order, 16 at a
+// time (their loads issued together), lane j adding column j (64 columns per
+// pass, KPC passes) in float64; gCS[v] += the total (ids that occur in no
+// block are untouched).
+template <int KPC>
+__global__ __launch_bounds__(256) void id_merge_kernel(
+    const int32_t *__restrict__ rid, const int32_t *__restrict__ first, int64_t nq, int64_t nblk,
+    const double *__restrict__ part, int kp, int64_t k, int64_t vocab, float *__restrict__ gCS,
+    int64_t ldgc) {
   const int lane = threadIdx.x & 63;
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (s >= meta[0]) return;
-  const int64_t v = seg_id[s];
-  const int q0 = seg_ch[s], q1 = seg_ch[s + 1];
-  for (int64_t j = lane; j < k; j += 64) {
-    double acc = 0.0;
-    for (int q = q0; q < q1; ++q) acc += part[static_cast<int64_t>(q) * kp + j];
-    gCS[v * ldgc + j] += static_cast<float>(acc);
+  const int64_t v = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (v >= vocab) return;
+  const int64_t q = v / kIdRange;
+  double acc[KPC];
+#pragma unroll
+  for (int c = 0; c < KPC; ++c) acc[c] = 0.0;
+  bool any = false;
+  for (int64_t c0 = 0; c0 < nblk; c0 += 64) {  // the same trip count in every lane
+    const int64_t b = c0 + lane;
+    int r = -1;
+    if (b < nblk) {
+      const int32_t *fb = first + b * (nq + 1) + q;
+      const int32_t *ids = rid + b * kBlk;
+      for (int rr = fb[0], hi = fb[1]; rr < hi; ++rr)
+        if (ids[rr] == v) r = rr;
+    }
+    uint64_t mask = __ballot(r >= 0);
+    any = any || mask != 0;
+    while (mask) {  // the blocks holding v, ascending, 16 at a time
+      int64_t row[16];
+      int cnt = 0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        row[i] = 0;
+        if (mask) {
+          const int l = __builtin_ctzll(mask);
+          mask &= mask - 1;
+          row[i] = (c0 + l) * kBlk + __shfl(r, l, 64);
+          ++cnt;
+        }
+      }
+      double x[16][KPC];
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int c = 0; c < KPC; ++c) {
+          const int j = 64 * c + lane;
+          x[i][c] = part[row[i] * kp + (j < kp ? j : kp - 1)];
+        }
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (i < cnt)
+#pragma unroll
+          for (int c = 0; c < KPC; ++c) acc[c] += x[i][c];
+    }
+  }
+  if (!any) return;
+#pragma unroll
+  for (int c = 0; c < KPC; ++c) {
+    const int j = 64 * c + lane;
+    if (j < k) gCS[v * ldgc + j] += static_cast<float>(acc[c]);
   }
 }
 
@@ -373,25 +326,21 @@ hipError_t launch_embed_backward(const PackLayout &L, const void *packed, const 
                      : launch_table_project_generic(L, packed, dX0, N, ldg, c32, P.kp, s);
   if (e != hipSuccess) return e;
   auto I = [&](size_t off) { return reinterpret_cast<int32_t *>(w + off); };
-  hist_kernel<<<dim3(static_cast<unsigned>(P.nblk)), kSortThreads, 0, s>>>(tok, N, vocab,
-                                                                           err_flag, I(P.off_cnt));
-  block_prefix_kernel<<<dim3(static_cast<unsigned>(ceil_div(vocab, 256))), 256, 0, s>>>(
-      I(P.off_cnt), P.nblk, vocab, I(P.off_cur), I(P.off_count));
-  tile_scan_kernel<<<dim3(static_cast<unsigned>(P.ntile)), kSortThreads, 0, s>>>(
-      vocab, I(P.off_cur), I(P.off_lz), I(P.off_lch), I(P.off_tiles), P.ntile);
-  tiles_scan_kernel<<<dim3(1), kSortThreads, 0, s>>>(N, I(P.off_tiles), P.ntile, I(P.off_segoff),
-                                                      I(P.off_segch), I(P.off_meta));
-  tile_write_kernel<<<dim3(static_cast<unsigned>(P.ntile)), kSortThreads, 0, s>>>(
-      vocab, nullptr, 0, I(P.off_cur), I(P.off_lz), I(P.off_lch), I(P.off_tiles), P.ntile,
-      I(P.off_segid), I(P.off_segoff), I(P.off_segch), I(P.off_cbeg), I(P.off_cend),
-      I(P.off_count));
-  place_kernel<<<dim3(static_cast<unsigned>(P.nblk)), kSortThreads, 0, s>>>(
-      tok, N, vocab, I(P.off_cnt), I(P.off_cur), I(P.off_order));
   double *part = reinterpret_cast<double *>(w + P.off_part);
-  chunk_sum_kernel<<<dim3(static_cast<unsigned>(ceil_div(P.maxchunk, 4))), 256, 0, s>>>(
-      c32, P.kp, I(P.off_order), I(P.off_cbeg), I(P.off_cend), I(P.off_meta), part);
-  seg_sum_kernel<<<dim3(static_cast<unsigned>(ceil_div(P.maxseg, 4))), 256, 0, s>>>(
-      part, P.kp, L.k, I(P.off_segid), I(P.off_segch), I(P.off_meta), gCS, ldgc);
+  block_runs_kernel<<<dim3(static_cast<unsigned>(P.nblk)), kBlk, 0, s>>>(
+      tok, N, vocab, err_flag, c32, static_cast<int>(P.kp), P.nq, I(P.off_rid), I(P.off_first),
+      part);
+  const dim3 mg(static_cast<unsigned>(ceil_div(vocab, 4)));
+#define SN_MERGE(KPC)                                                                       \
+  id_merge_kernel<KPC><<<mg, 256, 0, s>>>(I(P.off_rid), I(P.off_first), P.nq, P.nblk, part, \
+                                          static_cast<int>(P.kp), L.k, vocab, gCS, ldgc)
+  if (P.kp <= 64)
+    SN_MERGE(1);
+  else if (P.kp <= 128)
+    SN_MERGE(2);
+  else
+    SN_MERGE(4);
+#undef SN_MERGE
   return hipGetLastError();
 }
 
