@@ -168,11 +168,13 @@ __global__ __launch_bounds__(256) void reset_kernel(double *__restrict__ state, 
 // ---------------------------------------------------------------------------
 // Loss terms |g|^2 - |c|^2 + c D c^T of 64 rows per block, summed: the
 // block's coefficient rows are staged in LDS with coalesced loads (row stride
-// 16 KT + 1 words, so per-lane row reads hit distinct banks); wave w takes the
-// coefficient indices a = w, w + 4, ... of every row (lane = row), with D's row
-// a read by uniform loads (D is padded to 16 KT columns, and so are the rows:
-// the padding is zero on both sides); the four waves' sums meet in LDS in a
-// fixed order.  Blocks past the nlblk that hold rows write no loss term.
+// 16 KT + 1 words, so per-lane row reads hit distinct banks; rows past N are
+// zero).  Wave w takes rows 16 w .. 16 w + 15: R = C D for its 16 rows on the
+// matrix cores in fp32 (D symmetric, read as fp32 B fragments; D is ~1e-3 in
+// size, so fp32 products leave c D c^T within ~1e-7 of itself), then per row
+// |c|^2 in float64 and c . R in fp32, each summed over the 16 lanes of its
+// row group by a fixed butterfly; the rows' terms meet in a fixed-order block
+// sum.  Blocks past the nlblk that hold rows write no loss term.
 //
 // With frag, the same staged rows also give the token contraction's operand
 // F in the kfrag layout: per (operand part p, token step s, column tile t,
@@ -191,38 +193,50 @@ __global__ __launch_bounds__(256) void loss_kernel(const float *__restrict__ c32
   __shared__ float cs[64 * LDL];
   __shared__ double red[256];
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 64;
-  const int64_t nr = N - r0 < 64 ? N - r0 : 64;
-  for (int64_t e = threadIdx.x; e < nr * KP; e += 256)
-    cs[(e / KP) * LDL + e % KP] = c32[r0 * KP + e];
-  __syncthreads();
+  const int64_t nr = N - r0 < 64 ? (N - r0 > 0 ? N - r0 : 0) : 64;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, n = lane & 15;
+  // D's B fragments: lane (g, n) of step (a-tile at, b-step bs) holds
+  // D[4 bs + g][16 at + n]; loaded before the rows are staged
+  float dfr[KT][4 * KT];
+#pragma unroll
+  for (int at = 0; at < KT; ++at)
+#pragma unroll
+    for (int bs = 0; bs < 4 * KT; ++bs)
+      dfr[at][bs] = static_cast<float>(dgram[(4 * bs + g) * KP + 16 * at + n]);
+  for (int64_t e = threadIdx.x; e < 64 * KP; e += 256)
+    cs[(e / KP) * LDL + e % KP] = e < nr * KP ? c32[r0 * KP + e] : 0.0f;
+  __syncthreads();
   (void)k;  // rows and columns of D past k are zero, and so are c's
-  double cc = 0.0, q = 0.0;
-  if (lane < nr) {
-    const float *c = cs + lane * LDL;
-    double r[KP / 4];  // (D c)_a for a = w + 4 i
+  const float *crow = cs + (16 * w + n) * LDL;  // A operand: row 16 w + n
+  double cc[4] = {0.0, 0.0, 0.0, 0.0};
+  float qf[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < KP / 4; ++i) r[i] = 0.0;
-#pragma unroll 4
-    for (int b = 0; b < KP; ++b) {
-      const double cb = c[b];
+  for (int at = 0; at < KT; ++at) {
+    f32x4 rr = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < KP / 4; ++i) r[i] += dgram[(w + 4 * i) * KP + b] * cb;
-    }
+    for (int bs = 0; bs < 4 * KT; ++bs)
+      rr = __builtin_amdgcn_mfma_f32_16x16x4f32(crow[4 * bs + g], dfr[at][bs], rr, 0, 0, 0);
+    // lane (g, n): R[16 w + 4 g + i][16 at + n]
 #pragma unroll
-    for (int i = 0; i < KP / 4; ++i) {
-      const double ca = c[w + 4 * i];
-      cc += ca * ca;
-      q += ca * r[i];
+    for (int i = 0; i < 4; ++i) {
+      const float ca = cs[(16 * w + 4 * g + i) * LDL + 16 * at + n];
+      cc[i] += static_cast<double>(ca) * static_cast<double>(ca);
+      qf[i] = fmaf(ca, rr[i], qf[i]);
     }
   }
-  red[threadIdx.x] = q - cc;
-  __syncthreads();
   double l = 0.0;
-  if (w == 0 && lane < nr)
-    l = gsq[r0 + lane] + (((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane]);
-  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      cc[i] += __shfl_xor(cc[i], off, 64);
+      qf[i] += __shfl_xor(qf[i], off, 64);
+    }
+    const int64_t row = 16 * w + 4 * g + i;
+    if (n == 0 && row < nr) l += gsq[r0 + row] + (static_cast<double>(qf[i]) - cc[i]);
+  }
   const double tot = block_sum256(l, red);
   if (threadIdx.x == 0 && blockIdx.x < nlblk) part[blockIdx.x] = tot;
   if (!frag) return;
