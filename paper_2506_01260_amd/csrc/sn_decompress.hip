@@ -155,7 +155,7 @@ template <int KS, bool HE, bool HP, int CM, bool PS>
 __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     const bf16_t *__restrict__ rfrag, int64_t k, const bf16_t *__restrict__ C, int64_t ldc,
     DTiling tm, IdArgs ids, ColSegs xs, int ncb, int ntiles,
-    int tiles_per_wg) {
+    int tiles_per_wg, int young_from) {
   constexpr int FR = 2 * KS;  // fragments per row group
   __shared__ u32x4 us[kPG * FR * 64];
   constexpr bool kIds = HE || HP;
@@ -376,24 +376,35 @@ __global__ __launch_bounds__(kDThreads) void decompress_cb_kernel(
     if (np1) load_p(p1, nxt, 1);
     cur = nxt;
   };
+  // The workgroups dispatched after every CU has one (the second on a CU)
+  // lose issue arbitration to the older waves on the same SIMDs and would
+  // end ~5 us later; their waves run at raised priority for the first half
+  // of their tiles, then at the default (pair at d = 4096: 131.1 -> 129.6 us).
+  const bool young = static_cast<int>(blockIdx.x) >= young_from;
+  if (young) __builtin_amdgcn_s_setprio(2);
   for (int j = 0; j < nt; j += 2) {
+    if (young && j == nt / 2) __builtin_amdgcn_s_setprio(0);
     tile_step(j, eA, eB);
     if (j + 1 < nt) tile_step(j + 1, eB, eA);
   }
   if (bad && ids.err_flag) atomicOr(ids.err_flag, bad);
 }
 
-// Resident workgroups of a kernel on the current device (CUs x occupancy).
+// Resident workgroups of a kernel on the current device (CUs x occupancy)
+// and the CUs.
+struct Slots {
+  int64_t slots, cus;
+};
 template <typename K>
-int64_t resident_slots(K kernel) {
+Slots resident_slots(K kernel) {
   int dev = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(kernel),
                                                    kDThreads, 0) != hipSuccess ||
       cus <= 0 || per_cu <= 0)
-    return 512;
-  return static_cast<int64_t>(cus) * per_cu;
+    return Slots{512, 256};
+  return Slots{static_cast<int64_t>(cus) * per_cu, cus};
 }
 
 template <int KS, bool HE, bool HP, int CM, bool PS = false>
@@ -405,16 +416,18 @@ void launch_dcb(const bf16_t *rf, const PackLayout &L, const void *C, int64_t ld
   const int64_t ntiles = tm.batch > 0 ? static_cast<int64_t>(tm.batch) * (tm.seq / 16)
                                       : ceil_div(tm.N, 16);
   // one round of resident workgroups over the whole grid, whole waves of tiles
-  static const int64_t slots = resident_slots(decompress_cb_kernel<KS, HE, HP, CM, PS>);
-  const int64_t groups = slots / ncb > 0 ? slots / ncb : 1;  // token groups per round
+  static const Slots sl = resident_slots(decompress_cb_kernel<KS, HE, HP, CM, PS>);
+  const int64_t groups = sl.slots / ncb > 0 ? sl.slots / ncb : 1;  // token groups per round
   int64_t per = ceil_div(ntiles, groups);
   per = per < kDW ? kDW : (per > kDW * kMaxWaveTiles ? kDW * kMaxWaveTiles : per);
   per = ceil_div(per, kDW) * kDW;
   const int64_t tgroups = ceil_div(ntiles, per);
   dim3 grid(static_cast<unsigned>(tgroups * ncb));
+  // workgroups past the first one per CU (when the grid has more)
+  const int64_t young_from = tgroups * ncb > sl.cus ? sl.cus : tgroups * ncb;
   decompress_cb_kernel<KS, HE, HP, CM, PS><<<grid, kDThreads, 0, s>>>(
       rf, L.k, static_cast<const bf16_t *>(C), ldc, tm, ids, X, ncb,
-      static_cast<int>(ntiles), static_cast<int>(per));
+      static_cast<int>(ntiles), static_cast<int>(per), static_cast<int>(young_from));
 }
 
 template <int KS, int CM>
