@@ -415,6 +415,11 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
       lds_barrier();
       lds_barrier();
     }
+    if constexpr (EPI == kEpiGrass) {  // the compute waves' epilogue exchange
+      lds_barrier();
+      lds_barrier();
+      lds_barrier();
+    }
     return;
   }
 
@@ -509,9 +514,118 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
   }
 
   // epilogue: lane (g, n) holds C[token, 16 t + 4 g .. +3]
-  if constexpr (EPI == kEpiGrass) {  // the row's four lane partials, fixed order
+  if constexpr (EPI == kEpiGrass) {
+    // The row's loss term |g|^2 - |c|^2 + c D c^T (D = U^T U - I).  (D c)_a
+    // on the matrix cores in fp32: A = fragments of D (staged once per
+    // workgroup in LDS), B = the lane's own coefficients (contraction index
+    // b = 16 t + 4 g + i of step (t, i)), so lane (g, n) receives (D c)_a of
+    // token n for a = 16 at + 4 g + i, the same a as its acc[at][i]; D is
+    // ~1e-3 in size, fp32 keeps the term to ~1e-7 of itself.  |c|^2 and the
+    // sums in float64, the four lanes of a row and the workgroup's rows added
+    // in a fixed order.  LDS after the last stage: the coefficients
+    // [column][row of the workgroup] (for the operand), D's fragments, the
+    // waves' loss sums.
+    const int64_t Tg = T0 + wave;
+    const bool ok = Tg < ntiles && 16 * Tg + n < tm.N;
+    constexpr int RW = 16 * NW + 1;  // row stride in words: column reads spread over the banks
+    constexpr int CT_W = (16 * KT * RW + 3) & ~3;
+    constexpr int DF_W = KT * KT * 4 * 64;  // D fragments, [at][t][i][lane]
+    static_assert((CT_W + DF_W) * 4 + NW * 8 <= NB * G::buf_units * 16, "epilogue exchange fits");
+    float *cT = reinterpret_cast<float *>(lds);
+    float *dl = cT + CT_W;
+    double *wl = reinterpret_cast<double *>(dl + DF_W);
+    lds_barrier();  // every wave is past its last stage
+#pragma unroll
+    for (int t = 0; t < KT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cT[(16 * t + 4 * g + i) * RW + 16 * wave + n] = ok ? acc[t][i] : 0.0f;
+    // D[16 at + n'][16 t + 4 g' + i] for lane (g', n') of fragment (at, t, i)
+    for (int e = wave * 64 + lane; e < DF_W; e += 64 * NW) {
+      const int l2 = e & 63, f = e >> 6;
+      const int i = f & 3, t = (f >> 2) % KT, at = (f >> 2) / KT;
+      dl[e] = static_cast<float>(
+          go.dgram[(16 * at + (l2 & 15)) * (16 * KT) + 16 * t + 4 * (l2 >> 4) + i]);
+    }
+    lds_barrier();
+    double cc = 0.0;
+    float q = 0.0f;
+#pragma unroll
+    for (int at = 0; at < KT; ++at) {
+      f32x4 rr = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < KT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          rr = __builtin_amdgcn_mfma_f32_16x16x4f32(dl[((at * KT + t) * 4 + i) * 64 + lane],
+                                                    acc[t][i], rr, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        cc += static_cast<double>(acc[at][i]) * static_cast<double>(acc[at][i]);
+        q = fmaf(acc[at][i], rr[i], q);
+      }
+    }
     sq += __shfl_xor(sq, 16, 64);
     sq += __shfl_xor(sq, 32, 64);
+    cc += __shfl_xor(cc, 16, 64);
+    cc += __shfl_xor(cc, 32, 64);
+    q += __shfl_xor(q, 16, 64);
+    q += __shfl_xor(q, 32, 64);
+    double l = ok && g == 0 ? sq - cc + static_cast<double>(q) : 0.0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) l += __shfl_xor(l, off, 64);
+    if (lane == 0) wl[wave] = l;
+    if (go.frag) {
+      // slot (part p, 32-row step st of the workgroup, column tile t2, lane
+      // 16 g2 + n2): rows 32 st + 8 g2 + 0..7 of operand column 16 t2 + n2 (of
+      // 1 operand: C_hi for columns < k, C_lo of column - k below 2k; of 2:
+      // part 0 C_hi, part 1 C_lo), zero past k and past row N
+      constexpr int NST = NW / 2;
+      const int ktb = go.ktb, nparts = go.nparts;
+      const int64_t s_base = 16 * T0 / 32;
+      const int64_t per_part = (go.npad / 32) * ktb * 64;
+      const int nslots = nparts * NST * ktb * 64;
+      for (int sl = wave * 64 + lane; sl < nslots; sl += 64 * NW) {
+        const int p = sl / (NST * ktb * 64);
+        const int rem = sl - p * (NST * ktb * 64);
+        const int st = rem / (ktb * 64);
+        const int t2 = (rem / 64) % ktb;
+        const int l2 = rem & 63;
+        const int g2 = l2 >> 4, n2 = l2 & 15;
+        const int64_t c2 = 16 * t2 + n2;
+        bool lo;
+        int64_t col;
+        if (nparts == 1) {
+          lo = c2 >= k;
+          col = lo ? c2 - k : c2;
+        } else {
+          lo = p == 1;
+          col = c2;
+        }
+        const bool cvalid = col < k;
+        uint32_t wd[4];
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          bf16_t h[2];
+#pragma unroll
+          for (int e2 = 0; e2 < 2; ++e2) {
+            const int row = 32 * st + 8 * g2 + 2 * qq + e2;
+            const float x = cvalid ? cT[col * RW + row] : 0.0f;
+            const bf16_t hi = from_f32<bf16_t>(x);
+            h[e2] = lo ? from_f32<bf16_t>(x - to_f32(hi)) : hi;
+          }
+          wd[qq] = static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
+        }
+        const int64_t slot = p * per_part + ((s_base + st) * ktb + t2) * 64 + l2;
+        *reinterpret_cast<u32x4 *>(reinterpret_cast<bf16_t *>(go.frag) + slot * 8) =
+            u32x4{wd[0], wd[1], wd[2], wd[3]};
+      }
+    }
+    lds_barrier();
+    if (wave == 0 && lane == 0) {
+      double tot = 0.0;
+      for (int w2 = 0; w2 < NW; ++w2) tot += wl[w2];
+      go.part[blockIdx.x] = tot;
+    }
   }
   int64_t T = T0 + wave;
   if (T >= ntiles) return;  // a tile past the end computed a duplicate
@@ -520,10 +634,6 @@ __global__ __launch_bounds__(threads_c<NW>()) void compress_kernel(const bf16_t 
   if (tm.bp == 1 && i >= tm.N) return;
   if (tok >= tm.N) return;  // a row past N of a short last sequence
   if constexpr (EPI == kEpiGrass) {
-#pragma unroll
-    for (int t = 0; t < KT; ++t)
-      *reinterpret_cast<f32x4 *>(go.c32 + tok * go.kp + 16 * t + 4 * g) = acc[t];
-    if (g == 0) go.gsq[tok] = sq;
     if (!Cout) return;
   }
   if (EPI == kEpiProjected) {
@@ -893,6 +1003,24 @@ hipError_t launch_compress_projected_mfma(const PackLayout &L, const void *packe
                                           int64_t N, int64_t ldx, const ProjArgs &pa, void *C,
                                           int64_t ldc, hipStream_t s) {
   return launch_plain<kEpiProjected>(L, packed, X, N, ldx, pa, C, ldc, s);
+}
+
+int64_t grass_compress_groups(const PackLayout &L, int64_t N, int64_t *steps) {
+  int nw = 4;
+  switch (L.kt) {
+    case 1: nw = pick_nw<1, false, false, 1>(N); break;
+    case 2: nw = pick_nw<2, false, false, 1>(N); break;
+    case 3: nw = pick_nw<3, false, false, 1>(N); break;
+    case 4: nw = pick_nw<4, false, false, 1>(N); break;
+    case 5: nw = pick_nw<5, false, false, 1>(N); break;
+    case 6: nw = pick_nw<6, false, false, 1>(N); break;
+    case 7: nw = pick_nw<7, false, false, 1>(N); break;
+    case 8: nw = pick_nw<8, false, false, 1>(N); break;
+    default: break;
+  }
+  const int64_t groups = ceil_div(ceil_div(N, 16), nw);
+  if (steps) *steps = groups * (nw / 2);
+  return groups;
 }
 
 hipError_t launch_grass_compress_mfma(const PackLayout &L, const void *packed, const void *G,

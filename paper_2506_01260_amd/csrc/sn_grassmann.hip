@@ -15,14 +15,14 @@
 // packed basis) the row term is |g|^2 - |c|^2 + c D c^T.
 //
 // MFMA path (bf16, d a multiple of 64, k <= 128), per accumulate:
-//   1. the staged compress kernel with the subspace-update epilogue: C in
-//      fp32 (and bf16 for the wire when asked) and each row's |g|^2;
-//   2. loss_kernel: the rows' loss terms summed per 256 rows; frag_kernel: C
-//      split into bf16 hi + lo in the MFMA operand layout of a contraction
-//      over tokens;
-//   3. the weight projection's pass-1 kernel with tokens as the contraction:
+//   1. the staged compress kernel with the subspace-update epilogue: per row
+//      |g|^2 (summed with the stages), c = g U, and the loss term (c D c^T
+//      on the matrix cores), summed per workgroup; C split into bf16 hi + lo
+//      in the MFMA operand layout of a contraction over tokens (through
+//      LDS); C in bf16 for the wire when asked;
+//   2. the weight projection's pass-1 kernel with tokens as the contraction:
 //      Tp[split][i][j] = sum over the split's rows of C_hi/lo[n, j] G[n, i];
-//   4. finish_kernel: Y += the splits and halves in a fixed order (float64),
+//   3. finish_kernel: Y += the splits and halves in a fixed order (float64),
 //      the loss partials into the state's scalars.
 // Generic path (fp32, other shapes): float64 kernels with one thread per
 // output, the loss taken directly as sum (g - c U^T)^2.
@@ -48,8 +48,8 @@ struct AccPlan {
   int64_t rows = 0;    // tokens per split, a multiple of 128
   int64_t npad = 0;    // ds * rows >= N
   int64_t m_pad = 0;   // d rounded up to 128
-  int64_t nlblk = 0;   // loss blocks (64 rows on the MFMA path, 256 on the generic)
-  size_t off_c = 0, off_gsq = 0, off_frag = 0, off_part = 0, off_tp = 0, total = 0;
+  int64_t nlblk = 0;   // loss partials (at most one per 64 rows on the MFMA path, 256 on the generic)
+  size_t off_c = 0, off_frag = 0, off_part = 0, off_tp = 0, total = 0;
 };
 
 AccPlan acc_plan(const PackLayout &L, int64_t N, bool mfma) {
@@ -73,10 +73,6 @@ AccPlan acc_plan(const PackLayout &L, int64_t N, bool mfma) {
     P.ds = static_cast<int>(ceil_div(N > 0 ? N : 1, P.rows));
     P.npad = P.ds * P.rows;
     P.m_pad = ceil_div(L.d, 128) * 128;
-    P.off_c = off;
-    off = align256(off + static_cast<size_t>(N) * 16 * P.kt * 4);
-    P.off_gsq = off;
-    off = align256(off + static_cast<size_t>(N) * 8);
     P.off_frag = off;
     off = align256(off + static_cast<size_t>(P.nparts) * (P.npad / 32) * P.ktb * 1024);
     P.off_part = off;
@@ -166,145 +162,6 @@ __global__ __launch_bounds__(256) void reset_kernel(double *__restrict__ state, 
 // ---------------------------------------------------------------------------
 // accumulate, MFMA path
 // ---------------------------------------------------------------------------
-// Loss terms |g|^2 - |c|^2 + c D c^T of 64 rows per block, summed: the
-// block's coefficient rows are staged in LDS with coalesced loads (row stride
-// 16 KT + 1 words, so per-lane row reads hit distinct banks; rows past N are
-// zero).  Wave w takes rows 16 w .. 16 w + 15: R = C D for its 16 rows on the
-// matrix cores in fp32 (D symmetric, read as fp32 B fragments; D is ~1e-3 in
-// size, so fp32 products leave c D c^T within ~1e-7 of itself), then per row
-// |c|^2 in float64 and c . R in fp32, each summed over the 16 lanes of its
-// row group by a fixed butterfly; the rows' terms meet in a fixed-order block
-// sum.  Blocks past the nlblk that hold rows write no loss term.
-//
-// With frag, the same staged rows also give the token contraction's operand
-// F in the kfrag layout: per (operand part p, token step s, column tile t,
-// lane 16 g + n) the 8 bf16 F[32 s + 8 g + e, 16 t + n].  Column c of operand
-// 1 of 1 is C_hi[:, c] for c < k and C_lo[:, c - k] for k <= c < 2k; of 2
-// operands, part 0 is C_hi and part 1 C_lo.  Zero past the columns and past
-// row N (the grid then covers all npad rows).
-template <int KT>
-__global__ __launch_bounds__(256) void loss_kernel(const float *__restrict__ c32,
-                                                   const double *__restrict__ gsq,
-                                                   const double *__restrict__ dgram, int64_t N,
-                                                   int64_t k, double *__restrict__ part,
-                                                   int64_t nlblk, bf16_t *__restrict__ frag,
-                                                   int nparts, int ktb, int64_t npad) {
-  constexpr int KP = 16 * KT, LDL = KP + 1;
-  __shared__ float cs[64 * LDL];
-  __shared__ double red[256];
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 64;
-  const int64_t nr = N - r0 < 64 ? (N - r0 > 0 ? N - r0 : 0) : 64;
-  const int lane = threadIdx.x & 63;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, n = lane & 15;
-  // D's B fragments: lane (g, n) of step (a-tile at, b-step bs) holds
-  // D[4 bs + g][16 at + n]; loaded before the rows are staged
-  float dfr[KT][4 * KT];
-#pragma unroll
-  for (int at = 0; at < KT; ++at)
-#pragma unroll
-    for (int bs = 0; bs < 4 * KT; ++bs)
-      dfr[at][bs] = static_cast<float>(dgram[(4 * bs + g) * KP + 16 * at + n]);
-  for (int64_t e = threadIdx.x; e < 64 * KP; e += 256)
-    cs[(e / KP) * LDL + e % KP] = e < nr * KP ? c32[r0 * KP + e] : 0.0f;
-  __syncthreads();
-  (void)k;  // rows and columns of D past k are zero, and so are c's
-  const float *crow = cs + (16 * w + n) * LDL;  // A operand: row 16 w + n
-  double cc[4] = {0.0, 0.0, 0.0, 0.0};
-  float qf[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int at = 0; at < KT; ++at) {
-    f32x4 rr = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int bs = 0; bs < 4 * KT; ++bs)
-      rr = __builtin_amdgcn_mfma_f32_16x16x4f32(crow[4 * bs + g], dfr[at][bs], rr, 0, 0, 0);
-    // lane (g, n): R[16 w + 4 g + i][16 at + n]
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float ca = cs[(16 * w + 4 * g + i) * LDL + 16 * at + n];
-      cc[i] += static_cast<double>(ca) * static_cast<double>(ca);
-      qf[i] = fmaf(ca, rr[i], qf[i]);
-    }
-  }
-  double l = 0.0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      cc[i] += __shfl_xor(cc[i], off, 64);
-      qf[i] += __shfl_xor(qf[i], off, 64);
-    }
-    const int64_t row = 16 * w + 4 * g + i;
-    if (n == 0 && row < nr) l += gsq[r0 + row] + (static_cast<double>(qf[i]) - cc[i]);
-  }
-  const double tot = block_sum256(l, red);
-  if (threadIdx.x == 0 && blockIdx.x < nlblk) part[blockIdx.x] = tot;
-  if (!frag) return;
-  const int64_t per_part = (npad / 32) * ktb * 64;
-  const int nsl = nparts * 2 * ktb * 64;  // the block's two token steps
-  for (int sl = threadIdx.x; sl < nsl; sl += 256) {
-    const int p = sl / (2 * ktb * 64);
-    const int rem = sl - p * (2 * ktb * 64);
-    const int sb = rem / (ktb * 64);
-    const int t = (rem / 64) % ktb;
-    const int l2 = rem & 63;
-    const int g = l2 >> 4, n = l2 & 15;
-    const int64_t c2 = 16 * t + n;
-    bool lo;
-    int64_t col;
-    if (nparts == 1) {
-      lo = c2 >= k;
-      col = lo ? c2 - k : c2;
-    } else {
-      lo = p == 1;
-      col = c2;
-    }
-    const bool cvalid = col < k;
-    uint32_t wd[4];
-#pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
-      bf16_t h[2];
-#pragma unroll
-      for (int e2 = 0; e2 < 2; ++e2) {
-        const int lr = 32 * sb + 8 * g + 2 * qq + e2;  // row within the block
-        h[e2] = bf16_t(0);
-        if (cvalid && lr < nr) {
-          const float x = cs[lr * LDL + col];
-          const bf16_t hi = from_f32<bf16_t>(x);
-          h[e2] = lo ? from_f32<bf16_t>(x - to_f32(hi)) : hi;
-        }
-      }
-      wd[qq] = static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
-    }
-    const int64_t s = r0 / 32 + sb;
-    const int64_t slot = p * per_part + (s * ktb + t) * 64 + l2;
-    *reinterpret_cast<u32x4 *>(frag + slot * 8) = u32x4{wd[0], wd[1], wd[2], wd[3]};
-  }
-}
-
-// The loss terms, and with frag the token contraction's operand (npad a
-// multiple of 64: the grid then covers every operand row).
-hipError_t launch_loss(int kt, const float *c32, const double *gsq, const double *dgram,
-                       int64_t N, int64_t k, double *part, int64_t nlblk, bf16_t *frag,
-                       int nparts, int ktb, int64_t npad, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(frag ? npad / 64 : nlblk));
-#define SN_LOSS(KT) \
-  loss_kernel<KT><<<grid, 256, 0, s>>>(c32, gsq, dgram, N, k, part, nlblk, frag, nparts, ktb, npad)
-  switch (kt) {
-    case 1: SN_LOSS(1); break;
-    case 2: SN_LOSS(2); break;
-    case 3: SN_LOSS(3); break;
-    case 4: SN_LOSS(4); break;
-    case 5: SN_LOSS(5); break;
-    case 6: SN_LOSS(6); break;
-    case 7: SN_LOSS(7); break;
-    case 8: SN_LOSS(8); break;
-    default: return hipErrorNotSupported;
-  }
-#undef SN_LOSS
-  return hipGetLastError();
-}
-
 // ---------------------------------------------------------------------------
 // accumulate, generic path (float64, one thread per output)
 // ---------------------------------------------------------------------------
@@ -602,16 +459,29 @@ hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, cons
   const AccPlan P = acc_plan(L, N, mfma);
   double *part = reinterpret_cast<double *>(w + P.off_part);
   if (mfma) {
+    // the compress writes the loss partials (one per workgroup) and, for Y,
+    // the token contraction's operand; the operand's steps past its
+    // workgroups (npad > their rows) are zeroed here
+    bf16_t *frag = reinterpret_cast<bf16_t *>(w + P.off_frag);
     GrassOut go;
-    go.c32 = reinterpret_cast<float *>(w + P.off_c);
-    go.kp = 16 * P.kt;
-    go.gsq = reinterpret_cast<double *>(w + P.off_gsq);
+    go.dgram = reinterpret_cast<const double *>(base + L.off_gram);
+    go.part = part;
+    go.frag = with_su ? frag : nullptr;
+    go.nparts = P.nparts;
+    go.ktb = P.ktb;
+    go.npad = P.npad;
+    int64_t steps = 0;
+    const int64_t nlblk = grass_compress_groups(L, N, &steps);
     hipError_t e = launch_grass_compress_mfma(L, packed, G, N, ldg, go, Cwire, ldc, s);
     if (e != hipSuccess) return e;
-    bf16_t *frag = reinterpret_cast<bf16_t *>(w + P.off_frag);
-    e = launch_loss(P.kt, go.c32, go.gsq, reinterpret_cast<const double *>(base + L.off_gram),
-                    N, L.k, part, P.nlblk, with_su ? frag : nullptr, P.nparts, P.ktb, P.npad, s);
-    if (e != hipSuccess) return e;
+    if (with_su && steps < P.npad / 32) {
+      const int64_t per_part = (P.npad / 32) * P.ktb * 512;  // bf16 per operand
+      const int64_t tail = (P.npad / 32 - steps) * P.ktb * 512 / 4;  // as doubles
+      for (int p = 0; p < P.nparts; ++p) {
+        double *t0 = reinterpret_cast<double *>(frag + p * per_part + steps * P.ktb * 512);
+        reset_kernel<<<dim3(static_cast<unsigned>(ceil_div(tail, 256))), 256, 0, s>>>(t0, tail);
+      }
+    }
     float *tp = reinterpret_cast<float *>(w + P.off_tp);
     if (with_su) {
       const int64_t per_part = static_cast<int64_t>(P.npad / 32) * P.ktb * 512;
@@ -625,7 +495,7 @@ hipError_t launch_grass_accumulate(const PackLayout &L, const void *packed, cons
     }
     const int64_t nfin = with_su ? ceil_div(L.d * L.k, 256) : 1;
     finish_kernel<<<dim3(static_cast<unsigned>(nfin)), 256, 0, s>>>(
-        tp, P.ds, P.m_pad, 16 * P.ktb, P.nparts, L.d, L.k, with_su ? 1 : 0, part, P.nlblk,
+        tp, P.ds, P.m_pad, 16 * P.ktb, P.nparts, L.d, L.k, with_su ? 1 : 0, part, nlblk,
         with_su ? 1 : 0, st);
     return hipGetLastError();
   }

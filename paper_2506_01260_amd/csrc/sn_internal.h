@@ -148,17 +148,24 @@ hipError_t launch_compress_projected_generic(const PackLayout &L, const void *pa
 size_t project_workspace_mfma(int64_t d, int64_t k, int64_t m);
 
 // ---- subspace update (Sec. 4.5) ---------------------------------------------
-// Outputs of the compress epilogue that feeds the subspace update: fp32
-// coefficient rows (row stride kp = 16 ceil(k/16), zero past k) and each
-// row's sum of squares.
+// The compress epilogue that feeds the subspace update: each workgroup's sum
+// of the rows' loss terms |g|^2 - |c|^2 + c D c^T (D = U^T U - I, kp x kp
+// float64, kp = 16 ceil(k/16)) into part[workgroup], and with frag the token
+// contraction's operand (C split into bf16 hi + lo in the kfrag layout:
+// nparts operands of ktb column tiles and npad rows).
 struct GrassOut {
-  float *c32 = nullptr;
-  int64_t kp = 0;
-  double *gsq = nullptr;
+  const double *dgram = nullptr;
+  double *part = nullptr;
+  uint16_t *frag = nullptr;  // bf16 bits
+  int nparts = 0, ktb = 0;
+  int64_t npad = 0;
 };
 hipError_t launch_grass_compress_mfma(const PackLayout &L, const void *packed, const void *G,
                                       int64_t N, int64_t ldg, const GrassOut &go, void *Cwire,
                                       int64_t ldc, hipStream_t s);
+// Workgroups (loss partials) of that compress for N rows, and 32-row steps
+// of the operand it writes.
+int64_t grass_compress_groups(const PackLayout &L, int64_t N, int64_t *steps);
 // Tp[split][i][j] = sum over the split's token rows n of F[n, j] G[n, i]
 // (F in the kfrag layout with ktb column tiles and npad rows, zero past N).
 hipError_t launch_grass_tokens_mfma(const void *frag, int ktb, int64_t npad, const void *G,
