@@ -249,9 +249,10 @@ __device__ __forceinline__ void wait_vm_upto(int v) {
 // (C = X U - (P U)[pos] - (T_fixed U)[tok], the subtraction done on the k
 // coefficients of each token); fp32 rows of a projected table (padded to
 // 16 ceil(k/16) columns, zero past k).
-// The subspace-update epilogue (kEpiGrass) writes the fp32 coefficient rows
-// (padded like kEpiF32) and each row's sum of squares (fp64) for the
-// off-subspace loss, plus the bf16 coefficients when an output is given.
+// The subspace-update epilogue (kEpiGrass) sums each row's off-subspace loss
+// term per workgroup and writes the coefficients split into bf16 hi + lo in
+// the token contraction's operand layout, plus the bf16 coefficients when an
+// output is given (see GrassOut).
 enum Epi { kEpiBf16 = 0, kEpiProjected = 1, kEpiF32 = 2, kEpiGrass = 3 };
 
 template <int KT, bool HE, bool HP, int BP, int NW, int EPI>

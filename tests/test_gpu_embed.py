@@ -80,6 +80,37 @@ def test_backward_matches_oracle(dtype, d, k, vocab, batch, seq):
     assert_parity(got, ref, "f32", "gC_S accumulated")
 
 
+@pytest.mark.parametrize("pattern", ["one_id", "long_runs"])
+def test_backward_long_runs(pattern):
+    """Rows of one id that fill whole token blocks (runs crossing every wave
+    of a block, and every block), and an id that returns after a long run of
+    another: the per-id sums must still take every row exactly once."""
+    dtype, d, k, vocab, N = "bf16", 512, 40, 64, 3000  # last block partial
+    log(f"[embed backward] {pattern} N={N}")
+    cfg = synth.Config("embed", dtype, d, k, vocab, 1, N, True, 0.0, 1e-2)
+    b, _, _, dec = _setup(cfg)
+    U = dec(b["U"]).astype(np.float64)
+    if pattern == "one_id":
+        tok = np.full(N, 7, np.int32)
+    else:
+        tok = np.concatenate([np.full(1100, 3), np.full(900, 40), (np.arange(300) % 5) + 58,
+                              np.full(700, 3)]).astype(np.int32)
+    G = synth.make_gradient(0, N, cfg)
+    basis = sn.sn_basis_pack(dev(b["U"], dtype))
+    outs = []
+    for _ in range(2):
+        gCS = torch.zeros(vocab, k, device="cuda")
+        sn.sn_embed_lowrank_backward(basis, dev(G, dtype), ids(tok), gCS)
+        torch.cuda.synchronize()
+        outs.append(host(gCS))
+    assert np.array_equal(outs[0], outs[1]), "bitwise the same on every run"
+    grad = em.lowrank_grad(dec(G), U, tok, vocab)
+    present = np.zeros(vocab, bool)
+    present[tok] = True
+    assert np.all(outs[0][~present] == 0.0)
+    assert_parity(outs[0][present], grad[present], "f32", f"scatter of dX0 U, {pattern}")
+
+
 def test_backward_config2_zipf_deterministic():
     """Config 2's token stream (N = 32768, vocab 32000, Zipf(1.1)): one id
     holds ~14 % of the tokens; every row of the gradient, and two runs
