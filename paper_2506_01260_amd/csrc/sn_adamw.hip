@@ -21,6 +21,9 @@
 // sums added across the row groups in LDS in a fixed order); pass 2 adds the
 // blocks in a fixed order and forms alpha; pass 3 reads G again, updates M
 // and W (24 bytes per element: G is read twice, M once).
+// M, V and W are loaded and stored non-temporally (each is touched once per
+// step) and G normally, so the Infinity Cache keeps G for pass 3's second
+// read: subspace step on 4096 x 14336 bf16 298 -> 274 us, standard 252 -> 248.
 #include "sn_device.h"
 #include "sn_internal.h"
 
@@ -42,9 +45,24 @@ struct AdamArgs {
 };
 
 template <typename T> struct Vec8;
+// NT: non-temporal access (cache-policy hint), for data touched once per step.
+template <typename V, bool NT>
+__device__ __forceinline__ V ld_vec(const V *p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  return *p;
+}
+template <typename V, bool NT>
+__device__ __forceinline__ void st_vec(V *p, V v) {
+  if constexpr (NT)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
+}
+
 template <> struct Vec8<bf16_t> {
+  template <bool NT>
   static __device__ __forceinline__ void load(const bf16_t *p, float (&x)[8]) {
-    const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+    const u32x4 v = ld_vec<u32x4, NT>(reinterpret_cast<const u32x4 *>(p));
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -52,40 +70,44 @@ template <> struct Vec8<bf16_t> {
       x[2 * i + 1] = bf_hi(w[i]);
     }
   }
+  template <bool NT>
   static __device__ __forceinline__ void store(bf16_t *p, const float (&x)[8]) {
-    *reinterpret_cast<u32x4 *>(p) = u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
-                                          pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7])};
+    st_vec<u32x4, NT>(reinterpret_cast<u32x4 *>(p),
+                      u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                            pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7])});
   }
 };
 template <> struct Vec8<float> {
+  template <bool NT>
   static __device__ __forceinline__ void load(const float *p, float (&x)[8]) {
-    const f32x4 a = *reinterpret_cast<const f32x4 *>(p);
-    const f32x4 b = *reinterpret_cast<const f32x4 *>(p + 4);
+    const f32x4 a = ld_vec<f32x4, NT>(reinterpret_cast<const f32x4 *>(p));
+    const f32x4 b = ld_vec<f32x4, NT>(reinterpret_cast<const f32x4 *>(p + 4));
     x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
     x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
   }
+  template <bool NT>
   static __device__ __forceinline__ void store(float *p, const float (&x)[8]) {
-    *reinterpret_cast<f32x4 *>(p) = f32x4{x[0], x[1], x[2], x[3]};
-    *reinterpret_cast<f32x4 *>(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+    st_vec<f32x4, NT>(reinterpret_cast<f32x4 *>(p), f32x4{x[0], x[1], x[2], x[3]});
+    st_vec<f32x4, NT>(reinterpret_cast<f32x4 *>(p + 4), f32x4{x[4], x[5], x[6], x[7]});
   }
 };
 
 // 8 columns of one row: vector access when VEC (cols % 8 == 0, 16-byte
 // aligned rows), else element by element with a bound on the column
-template <typename T, bool VEC>
+template <typename T, bool VEC, bool NT = false>
 __device__ __forceinline__ void load8(const T *row, int64_t c0, int64_t cols, float (&x)[8]) {
   if constexpr (VEC) {
-    Vec8<T>::load(row + c0, x);
+    Vec8<T>::template load<NT>(row + c0, x);
   } else {
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = c0 + i < cols ? to_f32(row[c0 + i]) : 0.0f;
   }
 }
 
-template <typename T, bool VEC>
+template <typename T, bool VEC, bool NT = false>
 __device__ __forceinline__ void store8(T *row, int64_t c0, int64_t cols, const float (&x)[8]) {
   if constexpr (VEC) {
-    Vec8<T>::store(row + c0, x);
+    Vec8<T>::template store<NT>(row + c0, x);
   } else {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -114,26 +136,26 @@ __global__ __launch_bounds__(CT * RG) void moments_kernel(T *__restrict__ W, int
   auto row = [&](int64_t r) {
     float g[8], v[8];
     load8<T, VEC>(G + r * ldg, c0, cols, g);
-    load8<float, VEC>(V + r * ldm, c0, cols, v);
+    load8<float, VEC, true>(V + r * ldm, c0, cols, v);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = fmaf(a.b2, v[i], a.omb2 * (g[i] * g[i]));
-    store8<float, VEC>(V + r * ldm, c0, cols, v);
+    store8<float, VEC, true>(V + r * ldm, c0, cols, v);
     if constexpr (SUB) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[i] += v[i];
     } else {
       float m[8], w[8];
-      load8<float, VEC>(M + r * ldm, c0, cols, m);
+      load8<float, VEC, true>(M + r * ldm, c0, cols, m);
 #pragma unroll
       for (int i = 0; i < 8; ++i) m[i] = fmaf(a.b1, m[i], a.omb1 * g[i]);
-      store8<float, VEC>(M + r * ldm, c0, cols, m);
-      load8<T, VEC>(W + r * ldw, c0, cols, w);
+      store8<float, VEC, true>(M + r * ldm, c0, cols, m);
+      load8<T, VEC, true>(W + r * ldw, c0, cols, w);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const float alpha = 1.0f / (sqrtf(v[i] * a.inv_bc2) + a.eps);
         w[i] = w[i] - a.lr * alpha * (m[i] * a.inv_bc1) - a.wd * w[i];
       }
-      store8<T, VEC>(W + r * ldw, c0, cols, w);
+      store8<T, VEC, true>(W + r * ldw, c0, cols, w);
     }
   };
   // a full run of R rows is unrolled as one block (all its loads in flight
@@ -200,15 +222,15 @@ __global__ __launch_bounds__(CT * RG) void apply_kernel(T *__restrict__ W, int64
   auto row = [&](int64_t r) {
     float g[8], m[8], w[8];
     load8<T, VEC>(G + r * ldg, c0, cols, g);
-    load8<float, VEC>(M + r * ldm, c0, cols, m);
-    load8<T, VEC>(W + r * ldw, c0, cols, w);
+    load8<float, VEC, true>(M + r * ldm, c0, cols, m);
+    load8<T, VEC, true>(W + r * ldw, c0, cols, w);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       m[i] = fmaf(a.b1, m[i], a.omb1 * g[i]);
       w[i] = w[i] - al[i] * m[i] - a.wd * w[i];
     }
-    store8<float, VEC>(M + r * ldm, c0, cols, m);
-    store8<T, VEC>(W + r * ldw, c0, cols, w);
+    store8<float, VEC, true>(M + r * ldm, c0, cols, m);
+    store8<T, VEC, true>(W + r * ldw, c0, cols, w);
   };
   if (r1 - r0 == R) {
 #pragma unroll
