@@ -220,8 +220,8 @@ __global__ __launch_bounds__(kBlk) void block_runs_kernel(
 }
 
 // One wave per id v: lane L takes block c0 + L (64 blocks per pass) and finds
-// the block's run of id v through the range index (first[b][v / kIdRange]
-// ..); the blocks that hold v are then visited in ascending order, 16 at a
+// the block's run of id v by a binary search of the range index's runs
+// (first[b][v / kIdRange] ..); the blocks that hold v are then visited in ascending order, 16 at a
 // time (their loads issued together), lane j adding column j (64 columns per
 // pass, KPC passes) in float64; gCS[v] += the total (ids that occur in no
 // block are untouched).
@@ -242,10 +242,21 @@ __global__ __launch_bounds__(256) void id_merge_kernel(
     const int64_t b = c0 + lane;
     int r = -1;
     if (b < nblk) {
+      // the block's runs are in ascending id order: a binary search of the
+      // range (a linear scan waits on one load per run, and the ranges of the
+      // frequent ids hold tens of runs)
       const int32_t *fb = first + b * (nq + 1) + q;
       const int32_t *ids = rid + b * kBlk;
-      for (int rr = fb[0], hi = fb[1]; rr < hi; ++rr)
-        if (ids[rr] == v) r = rr;
+      int lo = fb[0], hi = fb[1];
+      const int end = hi;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (ids[mid] < v)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      if (lo < end && ids[lo] == v) r = lo;
     }
     uint64_t mask = __ballot(r >= 0);
     any = any || mask != 0;
