@@ -10,7 +10,7 @@
 //           coefficients dX0 U in fp32 (the compress kernel's fp32-row
 //           epilogue), then a deterministic sum by token id in two kernels:
 //           per block of 512 tokens, a bitonic sort of the (id, index) keys
-//           in LDS and, per run of equal ids, the float64 sum of its rows in
+//           and, per run of equal ids, the float64 sum of its rows in
 //           ascending token order; per id, the sum of its runs over the
 //           blocks in block order (float64), added to gC_S.
 #include "sn_device.h"
@@ -72,22 +72,23 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T *__restrict__ 
   C[idx] = CS[v * ldcs + j];
 }
 
-// Exclusive scan of one int per thread over the block's threads (Hillis-Steele
-// in LDS); *total receives the sum.
-__device__ int block_excl_scan(int v, int *buf, int *total) {
-  const int t = threadIdx.x;
-  buf[t] = v;
+// Exclusive count of the flags of the threads before this one in the block,
+// and the block's total: ballots within each wave, the waves' counts through
+// LDS (wtot holds kBlkWaves ints).
+__device__ int block_excl_count(bool flag, int *wtot, int *total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t m = __ballot(flag);
+  if (lane == 0) wtot[w] = __popcll(m);
   __syncthreads();
-  for (int off = 1; off < kBlk; off <<= 1) {
-    const int add = t >= off ? buf[t - off] : 0;
-    __syncthreads();
-    buf[t] += add;
-    __syncthreads();
+  int before = __popcll(m & ((1ull << lane) - 1ull)), all = 0;
+#pragma unroll
+  for (int i = 0; i < kBlkWaves; ++i) {
+    const int c = wtot[i];
+    before += i < w ? c : 0;
+    all += c;
   }
-  const int incl = buf[t];
-  *total = buf[kBlk - 1];
-  __syncthreads();
-  return incl - v;
+  *total = all;
+  return before;
 }
 
 __device__ __forceinline__ int clamp_tok(const int32_t *tok, int64_t i, int64_t vocab,
@@ -101,7 +102,7 @@ __device__ __forceinline__ int clamp_tok(const int32_t *tok, int64_t i, int64_t 
 }
 
 // Block b (tokens base .. base + 511): the keys (id << 9 | local index)
-// sorted in LDS (bitonic), so each run of equal ids lists its tokens in
+// sorted (bitonic), so each run of equal ids lists its tokens in
 // ascending order.  rid[b][r] = the id of run r (ascending); first[b][q] =
 // the first run with an id of at least q kIdRange (q = 0 .. nq, first[b][nq]
 // = the runs); part[b][r][:] = the float64 sum of the run's c32 rows in
@@ -117,32 +118,40 @@ __global__ __launch_bounds__(kBlk) void block_runs_kernel(
   __shared__ int rid[kBlk + 1];     // run of each sorted position (-1 past the end)
   __shared__ int rstart[kBlk + 1];  // first sorted position of each run
   __shared__ int runid[kBlk];       // id of each run
-  __shared__ int buf[kBlk];
+  __shared__ int wtot[kBlkWaves];
   __shared__ double piece[kBlkWaves][64];  // a wave's unfinished last run
   const int t = threadIdx.x;
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kBlk;
   const int nvalid = N - base < kBlk ? static_cast<int>(N - base) : kBlk;
-  key[t] = t < nvalid ? (static_cast<uint32_t>(clamp_tok(tok, base + t, vocab, err_flag)) << 9) |
-                            static_cast<uint32_t>(t)
-                      : 0xFFFFFFFFu;
-  __syncthreads();
+  // Bitonic sort, thread t holding position t: at each step it keeps the
+  // smaller or the larger of its key and its partner's (t ^ j), the smaller
+  // when it is the lower of the two in an ascending stage.  Partners in the
+  // same wave (j < 64) swap through cross-lane shuffles, the others through
+  // LDS (two barriers per such step, 6 of the 45 steps).
+  uint32_t kv = t < nvalid ? (static_cast<uint32_t>(clamp_tok(tok, base + t, vocab, err_flag)) << 9) |
+                                 static_cast<uint32_t>(t)
+                           : 0xFFFFFFFFu;
   for (int kk = 2; kk <= kBlk; kk <<= 1) {
     for (int j = kk >> 1; j > 0; j >>= 1) {
-      const int p = t ^ j;
-      if (p > t) {
-        const uint32_t a = key[t], b = key[p];
-        if ((a > b) == ((t & kk) == 0)) {
-          key[t] = b;
-          key[p] = a;
-        }
+      uint32_t pv;
+      if (j >= 64) {  // block-uniform branch
+        key[t] = kv;
+        __syncthreads();
+        pv = key[t ^ j];
+        __syncthreads();
+      } else {
+        pv = static_cast<uint32_t>(__shfl_xor(static_cast<int>(kv), j, 64));
       }
-      __syncthreads();
+      const bool keep_min = ((t & j) == 0) == ((t & kk) == 0);
+      kv = keep_min ? (kv < pv ? kv : pv) : (kv < pv ? pv : kv);
     }
   }
-  const uint32_t me = key[t];
+  key[t] = kv;
+  __syncthreads();
+  const uint32_t me = kv;
   const bool head = t < nvalid && (t == 0 || (key[t - 1] >> 9) != (me >> 9));
   int nrun = 0;
-  const int before = block_excl_scan(head ? 1 : 0, buf, &nrun);
+  const int before = block_excl_count(head, wtot, &nrun);
   rid[t] = t < nvalid ? (head ? before : before - 1) : -1;
   if (head) {
     rstart[before] = t;
@@ -154,14 +163,21 @@ __global__ __launch_bounds__(kBlk) void block_runs_kernel(
     rstart[nrun] = nvalid;
   }
   __syncthreads();
-  {  // the range index: run r is the first of the ranges after its predecessor's
+  {  // the range index: fb[q] = the first run with an id of at least q kIdRange
+     // (a binary search of the ascending run ids per q, the q spread over
+     // the threads)
     int32_t *fb = first + static_cast<int64_t>(blockIdx.x) * (nq + 1);
-    if (t < nrun) {
-      const int64_t q1 = runid[t] / kIdRange;
-      const int64_t q0 = t == 0 ? 0 : runid[t - 1] / kIdRange + 1;
-      for (int64_t q = q0; q <= q1; ++q) fb[q] = t;
-      if (t == nrun - 1)
-        for (int64_t q = q1 + 1; q <= nq; ++q) fb[q] = nrun;
+    for (int64_t q = t; q <= nq; q += kBlk) {
+      const int64_t target = q * kIdRange;
+      int lo = 0, hi = nrun;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (runid[mid] < target)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      fb[q] = lo;
     }
   }
 
