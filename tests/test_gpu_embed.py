@@ -111,6 +111,29 @@ def test_backward_long_runs(pattern):
     assert_parity(outs[0][present], grad[present], "f32", f"scatter of dX0 U, {pattern}")
 
 
+def test_backward_large_vocab():
+    """A Llama-3-sized vocabulary (128256 ids: 2004 id ranges in each block's
+    range index) with Zipf ids over 5 blocks and a partial sixth."""
+    dtype, d, k, vocab, N = "bf16", 256, 82, 128256, 2900
+    log(f"[embed backward] large vocab {vocab} k={k} N={N}")
+    cfg = synth.Config("embed", dtype, d, k, vocab, 1, N, True, 0.0, 1e-2)
+    b = synth.make_basis(0, cfg)
+    dec = lambda a: oracle.decode_bf16(a, np.float32)  # noqa: E731
+    U = dec(b["U"]).astype(np.float64)
+    tok = synth.make_ids(0, None, cfg)["tok"]
+    G = synth.make_gradient(0, N, cfg)
+    basis = sn.sn_basis_pack(dev(b["U"], dtype))
+    gCS = torch.zeros(vocab, k, device="cuda")
+    sn.sn_embed_lowrank_backward(basis, dev(G, dtype), ids(tok), gCS)
+    torch.cuda.synchronize()
+    got = host(gCS)
+    grad = em.lowrank_grad(dec(G), U, tok, vocab)
+    present = np.zeros(vocab, bool)
+    present[tok] = True
+    assert np.all(got[~present] == 0.0)
+    assert_parity(got[present], grad[present], "f32", "scatter of dX0 U, large vocabulary")
+
+
 def test_backward_config2_zipf_deterministic():
     """Config 2's token stream (N = 32768, vocab 32000, Zipf(1.1)): one id
     holds ~14 % of the tokens; every row of the gradient, and two runs
